@@ -1,0 +1,364 @@
+#!/usr/bin/env python3
+"""Benchmark of the weight-streaming read path on one MI355X.
+
+Headline: the batch-1 decode weight sweep of a synthetic Llama-70B-shaped model in bf16 (80 layers,
+d 8192, 64 q / 8 kv heads of dim 128, FFN 28672, vocab 128256; 139.0 GB of weights read per token),
+fully HBM-resident; one step = one decode token = one persistent launch over every matrix.
+`value` is the achieved weight-read rate in GB/s (decimal), counting each weight byte once.
+
+Also measured in the same run and reported under "rows" (same JSON line):
+  probe        pure-read reference, 1 GiB fp32 -> fp64 sum, HBM-resident and host-mapped
+  gemv_f16     4096 x 4096 fp16 GEMV, 32 distinct matrices visited per pass (1 GiB)
+  llama8b_q4   decode sweep of the Llama-3-8B shape in 4-bit blocks (4.22 GB per token)
+  size_sweep   bf16 GEMV with K = 4096 and N = 256 ... 140800 rows, resident and host-mapped
+  bus          pinned host -> device copy rate, the ceiling of every host-mapped arm
+
+Usage: python bench.py [--gpus 1] [--steps 16] [--warmup 2] [--rows probe,gemv_f16,...]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK = 8.0e12   # B/s, MI355X HBM3E
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=16, help="timed decode tokens of the headline")
+    p.add_argument("--warmup", type=int, default=2, help="untimed decode tokens before timing")
+    p.add_argument("--workload", default="llama70b_bf16", choices=["llama70b_bf16", "llama8b_q4"])
+    p.add_argument("--rows", default="probe,gemv_f16,llama8b_q4,size_sweep,bus",
+                   help="comma list of extra rows ('' for none)")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time of the sample")
+    return p.parse_args()
+
+
+# --------------------------------------------------------------------------------------------------
+# timing helpers (events on the stream the kernels are launched on)
+
+def timed(fn, reps, stream):
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / 1e3   # seconds
+
+
+def median_of(fn, reps, passes, stream):
+    return float(np.median([timed(fn, reps, stream) for _ in range(passes)]))
+
+
+# --------------------------------------------------------------------------------------------------
+# decode sweep
+
+SWEEPS = {"llama70b_bf16": ("LLAMA_70B", "bf16"), "llama8b_q4": ("LLAMA3_8B", "q4")}
+
+
+def sweep_workload(name, tokens_needed, stream, wsr, check_rows=16):
+    import torch
+    from synth import device as dv
+    from synth import workloads as wl
+    shape = getattr(wl, SWEEPS[name][0])
+    fmt = SWEEPS[name][1]
+    mats = wl.decode_matrices(shape)
+    t0 = time.time()
+    inp = dv.SweepInputs(mats, [fmt] * len(mats), tokens=tokens_needed)
+    log(f"{name}: {len(mats)} matrices, {inp.weight_bytes() / 1e9:.2f} GB generated and resident "
+        f"in {time.time() - t0:.1f} s")
+    specs = wsr.make_mats(inp.specs())
+    ws = torch.zeros(wsr.wsr_sweep_workspace_bytes(specs), dtype=torch.uint8, device="cuda")
+    return shape, fmt, mats, inp, specs, ws
+
+
+def run_sweep(name, steps, warmup, stream, wsr, want_cpu, cpu_seconds):
+    import torch
+    from synth import workloads as wl
+    shape, fmt, mats, inp, specs, ws = sweep_workload(name, max(steps, warmup, 1), stream, wsr)
+    bpt = inp.weight_bytes()
+    assert bpt == wl.bytes_per_token(shape, fmt)
+    if warmup:
+        wsr.wsr_decode_sweep(specs, warmup, ws, ws.numel(), stream)
+    torch.cuda.synchronize()
+    sec = timed(lambda: wsr.wsr_decode_sweep(specs, steps, ws, ws.numel(), stream), 1, stream)
+    per_tok = sec / steps
+    gbps = bpt / per_tok / 1e9
+    log(f"{name}: {steps} tokens in {sec * 1e3:.2f} ms -> {per_tok * 1e3:.3f} ms/token, "
+        f"{gbps:.1f} GB/s ({gbps * 1e9 / HBM_PEAK * 100:.1f}% of 8 TB/s), {1 / per_tok:.2f} tok/s")
+    parity = check_sweep(inp, [0, steps - 1])
+    log(f"{name}: parity on sampled rows: worst rel-L2 {parity['worst_rel_l2']:.2e}")
+    out = {"workload": name, "bytes_per_token": bpt, "footprint_bytes": wl.footprint_bytes(shape, fmt),
+           "tokens_timed": steps, "warmup_tokens": warmup, "ms_per_token": per_tok * 1e3,
+           "GBps": gbps, "hbm_frac": gbps * 1e9 / HBM_PEAK, "tokens_per_s": 1 / per_tok,
+           "launches_per_token": 1, "parity": parity}
+    if want_cpu:
+        out["cpu_baseline"] = cpu_baseline(inp, bpt, cpu_seconds)
+    del specs, ws, inp
+    torch.cuda.empty_cache()
+    return out
+
+
+def check_sweep(inp, tokens, nrows=8):
+    """Sampled rows of every matrix (first, last and spread rows) against the oracle."""
+    import oracle
+    from synth import workloads as wl
+    ora = oracle.get()
+    worst, n = 0.0, 0
+    ys = {}
+    for i, m in enumerate(inp.mats):
+        rows = np.unique(np.linspace(0, m.M - 1, nrows).astype(np.int64))
+        ys[i] = inp.y[i][tokens].cpu().numpy()
+        for t_i, t in enumerate(tokens):
+            x = inp.host_x(i, t)
+            got = ys[i][t_i][rows].astype(np.float64)
+            want = []
+            for r in rows:
+                hw = inp.host_weights(i, int(r), 1)
+                want.append((ora.gemv_q4(*hw, x) if inp.fmts[i] == wl.Q4 else ora.gemv16(hw, x, inp.fmts[i]))[0])
+            want = np.array(want)
+            err = float(np.linalg.norm(got - want) / max(np.linalg.norm(want), 1e-30))
+            worst = max(worst, err)
+            n += rows.size
+    return {"worst_rel_l2": worst, "rows_checked": n, "tokens_checked": list(tokens), "tol": 2e-3,
+            "ok": worst <= 2e-3}
+
+
+def cpu_baseline(inp, bpt, seconds):
+    """The oracle as it stands, all host cores, on the first matrices of token 0 until about
+    `seconds` of oracle time; scaled to the whole token."""
+    import oracle
+    from synth import workloads as wl
+    ora = oracle.get()
+    try:
+        threads = len(os.sched_getaffinity(0))
+    except AttributeError:
+        threads = os.cpu_count() or 1
+    threads = min(threads, 16)
+    spent, nbytes, names = 0.0, 0, []
+    for i, m in enumerate(inp.mats):
+        hw = inp.host_weights(i)
+        x = inp.host_x(i, 0)
+        t0 = time.perf_counter()
+        if inp.fmts[i] == wl.Q4:
+            ora.gemv_q4(*hw, x, threads=threads)
+        else:
+            ora.gemv16(hw, x, inp.fmts[i], threads=threads)
+        spent += time.perf_counter() - t0
+        nbytes += wl.matrix_bytes(m.M, m.K, inp.fmts[i])
+        names.append(f"L{m.layer}.{m.name}")
+        if spent >= seconds:
+            break
+    rate = nbytes / spent
+    log(f"cpu oracle: {nbytes / 1e9:.2f} GB in {spent:.1f} s on {threads} threads -> {rate / 1e9:.2f} GB/s")
+    return {"value": rate / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "tokens_per_s": rate / bpt, "seconds": spent,
+            "sample": f"token 0, first {len(names)} matrices in sweep order ({names[0]} .. {names[-1]}), "
+                      f"{nbytes / 1e9:.2f} GB of weights, fp64 oracle with OpenMP over rows"}
+
+
+# --------------------------------------------------------------------------------------------------
+# extra rows
+
+def row_probe(stream, wsr):
+    import torch
+    import synth
+    from synth import device as dv
+    from synth import workloads as wl
+    n = wl.PROBE_N
+    nb = n * 4
+    bufs = [dv.to_device(synth.grid_f32(n, seed=0, stream=1 + k)) for k in range(4)]
+    out = torch.zeros(1, dtype=torch.float64, device="cuda")
+    ws = torch.zeros(wsr.wsr_probe_workspace_bytes(n), dtype=torch.uint8, device="cuda")
+    call = lambda b: wsr.wsr_probe_read(b, n, out, ws, ws.numel(), stream)
+    for b in bufs:
+        call(b)
+    same = median_of(lambda: call(bufs[0]), 20, 5, stream) / 20
+    k = [0]
+
+    def rot():
+        call(bufs[k[0] & 3])
+        k[0] += 1
+    rotated = median_of(rot, 20, 5, stream) / 20
+    res = {"bytes": nb, "resident_GBps": nb / rotated / 1e9, "resident_same_buffer_GBps": nb / same / 1e9,
+           "resident_us": rotated * 1e6}
+    del bufs
+    torch.cuda.empty_cache()
+    # host-mapped: the same kernel over pinned host pages read in place across PCIe
+    host = torch.empty(nb, dtype=torch.uint8, pin_memory=True)
+    synth.grid_f32(n, seed=0, stream=1, out=host.numpy().view(np.float32))
+    dev, granted = wsr.wsr_register_host(host, nb, 0)
+    try:
+        call(dev)
+        mapped = median_of(lambda: call(dev), 2, 3, stream) / 2
+        res.update({"mapped_GBps": nb / mapped / 1e9, "mapped_registration": granted})
+    finally:
+        wsr.wsr_unregister_host(host)
+    log(f"probe: resident {res['resident_GBps']:.1f} GB/s (same buffer {res['resident_same_buffer_GBps']:.1f}), "
+        f"host-mapped {res['mapped_GBps']:.1f} GB/s")
+    return res
+
+
+def row_gemv_f16(stream, wsr):
+    import torch
+    import synth
+    from synth import device as dv
+    from synth import workloads as wl
+    cfg = wl.GemvConfig()
+    Ws = [dv.to_device(synth.normal16((cfg.M, cfg.K), wl.W_SIGMA, "f16", seed=0, stream=1 + b))
+          for b in range(cfg.rotate)]
+    x = dv.to_device(synth.normal16(cfg.K, wl.X_SIGMA, "f16", seed=0, stream=1000))
+    y = torch.empty((cfg.rotate, cfg.M), dtype=torch.float32, device="cuda")
+    bytes_one = cfg.M * cfg.K * 2
+
+    def pass_():
+        for b in range(cfg.rotate):
+            wsr.wsr_gemv_f16(Ws[b], x, y[b], cfg.M, cfg.K, wsr.WSR_F16, stream)
+    pass_()
+    t = median_of(pass_, 1, 15, stream)
+    per = t / cfg.rotate
+    # the same 32 matrices as one persistent launch
+    specs = wsr.make_mats([dict(fmt=1, M=cfg.M, K=cfg.K, w=Ws[b], x=x, y=y[b]) for b in range(cfg.rotate)])
+    ws = torch.zeros(wsr.wsr_sweep_workspace_bytes(specs), dtype=torch.uint8, device="cuda")
+    wsr.wsr_decode_sweep(specs, 1, ws, ws.numel(), stream)
+    tf = median_of(lambda: wsr.wsr_decode_sweep(specs, 1, ws, ws.numel(), stream), 1, 15, stream)
+    res = {"bytes_per_gemv": bytes_one, "us_per_gemv": per * 1e6, "GBps_per_dispatch": bytes_one / per / 1e9,
+           "one_launch_32_matrices_GBps": bytes_one * cfg.rotate / tf / 1e9}
+    log(f"gemv_f16 4096x4096: {per * 1e6:.2f} us/GEMV ({res['GBps_per_dispatch']:.1f} GB/s over 32 dispatches); "
+        f"one launch over all 32: {res['one_launch_32_matrices_GBps']:.1f} GB/s")
+    del Ws
+    torch.cuda.empty_cache()
+    return res
+
+
+def row_size_sweep(stream, wsr):
+    import torch
+    import synth
+    from synth import device as dv
+    from synth import workloads as wl
+    K = wl.SWEEP_K
+    x = dv.to_device(synth.normal16(K, wl.X_SIGMA, "bf16", seed=0, stream=2))
+    out = []
+    maxN = max(wl.SWEEP_N)
+    host = torch.empty(maxN * K * 2, dtype=torch.uint8, pin_memory=True)
+    synth.normal16(maxN * K, wl.W_SIGMA, "bf16", seed=0, stream=1, out=host.numpy().view(np.uint16))
+    hdev, granted = wsr.wsr_register_host(host, host.numel(), 0)
+    try:
+        for N in wl.SWEEP_N:
+            nbytes = N * K * 2
+            rot = max(1, -(-(1 << 30) // nbytes))   # distinct buffers per pass: at least 1 GiB
+            Ws = [torch.empty(N * K, dtype=torch.int16, device="cuda") for _ in range(rot)]
+            for W in Ws:
+                W.view(torch.uint8).copy_(host[:nbytes], non_blocking=True)
+            y = torch.empty(N, dtype=torch.float32, device="cuda")
+            k = [0]
+
+            def res_call():
+                wsr.wsr_gemv_f16(Ws[k[0] % rot], x, y, N, K, wsr.WSR_BF16, stream)
+                k[0] += 1
+            res_call()
+            reps = max(rot, 8)
+            tr = median_of(res_call, reps, 5, stream) / reps
+            ts = median_of(lambda: wsr.wsr_gemv_f16(Ws[0], x, y, N, K, wsr.WSR_BF16, stream), 8, 5, stream) / 8
+            tm = median_of(lambda: wsr.wsr_gemv_f16(hdev, x, y, N, K, wsr.WSR_BF16, stream), 1, 3, stream)
+            out.append({"N": N, "bytes": nbytes, "resident_GBps": nbytes / tr / 1e9,
+                        "resident_same_buffer_GBps": nbytes / ts / 1e9, "mapped_GBps": nbytes / tm / 1e9,
+                        "resident_us": tr * 1e6})
+            log(f"size sweep N={N:6d} ({nbytes / 2**20:7.1f} MiB): resident {nbytes / tr / 1e9:7.1f} GB/s, "
+                f"same-buffer {nbytes / ts / 1e9:7.1f}, host-mapped {nbytes / tm / 1e9:6.1f}")
+            del Ws
+            torch.cuda.empty_cache()
+    finally:
+        wsr.wsr_unregister_host(host)
+    return out
+
+
+def row_bus(stream):
+    import torch
+    n = 1 << 30
+    h = torch.empty(n, dtype=torch.uint8, pin_memory=True)
+    d = torch.empty(n, dtype=torch.uint8, device="cuda")
+    d.copy_(h, non_blocking=True)
+    t = median_of(lambda: d.copy_(h, non_blocking=True), 1, 5, stream)
+    log(f"bus: pinned host->device copy {n / t / 1e9:.1f} GB/s")
+    return {"h2d_GBps": n / t / 1e9}
+
+
+# --------------------------------------------------------------------------------------------------
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build measures one GPU: the weight-streaming path has no "
+                                   "multi-GPU form here (a sharded run would split rows across GPUs); "
+                                   "run with --gpus 1"}))
+        sys.exit(2)
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    from paper_2608_12114_amd import wsr
+    torch.cuda.set_device(0)
+    stream = torch.cuda.current_stream()
+    t_start = time.time()
+
+    head = run_sweep(args.workload, args.steps, args.warmup, stream, wsr, not args.no_cpu_baseline,
+                     args.cpu_seconds)
+    rows = {}
+    for r in [r for r in args.rows.split(",") if r]:
+        if r == "probe":
+            rows[r] = row_probe(stream, wsr)
+        elif r == "gemv_f16":
+            rows[r] = row_gemv_f16(stream, wsr)
+        elif r == "llama8b_q4":
+            if args.workload != "llama8b_q4":
+                rows[r] = run_sweep("llama8b_q4", 64, 4, stream, wsr, False, 0)
+        elif r == "size_sweep":
+            rows[r] = row_size_sweep(stream, wsr)
+        elif r == "bus":
+            rows[r] = row_bus(stream)
+        else:
+            raise SystemExit(f"unknown row {r}")
+
+    gbps = head["GBps"]
+    dtype = {"llama70b_bf16": "bf16", "llama8b_q4": "q4+f16"}[args.workload]
+    line = {
+        "metric": "achieved GB/s (% of HBM peak) for decode-step GEMV sweep; tokens/s at batch 1",
+        "value": round(gbps, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(head["ms_per_token"], 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": dtype, "data": "synthetic",
+        "config": {"workload": {"llama70b_bf16": "Llama-70B-shaped bf16 decode weight sweep, batch 1",
+                                "llama8b_q4": "Llama-3-8B-shaped q4 decode weight sweep, batch 1"}[args.workload],
+                   "layers": {"llama70b_bf16": 80, "llama8b_q4": 32}[args.workload],
+                   "bytes_per_token": head["bytes_per_token"], "residency": "HBM",
+                   "step": "one decode token: every projection matrix of every layer plus lm_head, one launch"},
+        "tokens_per_s": round(head["tokens_per_s"], 3), "hbm_frac": round(head["hbm_frac"], 4),
+        "roofline": {"bound": "hbm", "achieved": round(gbps, 2), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+                     "frac": round(head["hbm_frac"], 4), "traffic": None,
+                     "kernel": f"k_sweep ({dtype})", "bytes_per_launch": head["bytes_per_token"]},
+        "cpu_baseline": head.get("cpu_baseline"),
+        "parity": head["parity"],
+        "rows": rows,
+        "wall_s": round(time.time() - t_start, 1),
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,155 @@
+/*
+ * wsr.h - weight-streaming read kernels for AMD Instinct MI355X (gfx950): the C ABI.
+ *
+ * The operations are the ones "The Ingestion Tax: Adopting File-Backed Weights in Tensor
+ * Frameworks" measures: a batch-1 decode step rereads every weight byte once per token (Sec. 1,
+ * Sec. 6.2), the single-token GEMV of the matched protocol (Sec. 3.1), the pure-read reference that
+ * sets its ceiling (Sec. 3.1, Sec. 3.3), and the same kernels over host pages mapped into the GPU's
+ * address space (Sec. 5.1, Alg. 1; Sec. 7.3 for a discrete GPU on PCIe).
+ *
+ * Conventions shared by every entry point:
+ *  - Each call returns a wsr_status.  Arguments are checked before anything is enqueued: on any
+ *    status other than WSR_OK nothing was enqueued, except WSR_E_HIP from a failed kernel launch,
+ *    which may follow launches the same call already made.  A message for the calling thread is
+ *    available from wsr_last_error().  No call aborts or exits.
+ *  - Compute calls only enqueue work on the caller's HIP stream (`stream` is a hipStream_t; NULL
+ *    means the null stream of the current device) and return without waiting for the device: the
+ *    execution contract's C3, ordering on the GPU with no host drain (Sec. 2.2, Table 1).  Results
+ *    stay in device-visible memory (C2).  Kernels run on the current HIP device, which must be the
+ *    stream's device.
+ *  - The library never allocates, frees or retains caller memory.  Every pointer is caller-owned and
+ *    must stay valid until the stream has passed the enqueued work.  Weights and inputs are only
+ *    read (`const`); the library writes only the outputs (y, *sum_dev) and the workspace (ws).
+ *  - Device pointers may point to HBM or to host memory made device-visible (see
+ *    wsr_register_host); the kernels are the same either way.
+ *  - Sizes are element counts unless a name ends in `_bytes`.  Matrices are row-major (M, K) with
+ *    strides (K, 1), as in Alg. 1.
+ *  - Results are deterministic: a given input and shape always gives bitwise-identical output,
+ *    whatever memory the operands live in.
+ *  - Not thread-safe per workspace: concurrent calls must use distinct workspaces.
+ */
+#ifndef WSR_H
+#define WSR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define WSR_ABI_VERSION 1
+
+typedef enum {
+    WSR_OK = 0,
+    WSR_E_ARG = 1,          /* null pointer, negative size, unknown format or flag, n_tokens < 1  */
+    WSR_E_ALIGN = 2,        /* host range base or length not a page multiple (Alg. 1's reject
+                               rule); device operand misaligned; K % 8 != 0 (16-bit) or
+                               K % 32 != 0 (q4)                                                  */
+    WSR_E_SIZE = 3,         /* workspace too small, or a size whose byte count overflows        */
+    WSR_E_UNSUPPORTED = 4,  /* the runtime refused a request, e.g. pinning an existing host range
+                               (distinct from a failed HIP call, Sec. 7.3)                      */
+    WSR_E_STATE = 5,        /* range already registered, or unregister of an unknown range      */
+    WSR_E_HIP = 6           /* a HIP runtime call or kernel launch failed                       */
+} wsr_status;
+
+typedef enum {
+    WSR_F16 = 1,    /* IEEE binary16                                                          */
+    WSR_BF16 = 2,   /* bfloat16                                                               */
+    WSR_Q4 = 3      /* blocks of 32 signed int4 weights sharing one fp16 scale (see gemv_q4)   */
+} wsr_fmt;
+
+/* Message describing the last failed call on this thread ("" if none). */
+const char* wsr_last_error(void);
+
+/* WSR_ABI_VERSION of the library actually loaded. */
+int wsr_abi_version(void);
+
+/* ---- host memory read in place -------------------------------------------------------------
+
+   wsr_register_host: make host range [host, host + bytes) readable by the kernels and return its
+   device address.  Follows the producer of Alg. 1 (Sec. 5.1): the range must start on a page
+   boundary and its length must be a whole number of pages (else WSR_E_ALIGN: a partial page would
+   alias a neighbouring tensor); one call yields one registration and nothing is cached by address
+   (WSR_E_STATE if [host] is already registered).
+   - A range already device-visible (pinned host memory from hipHostMalloc, e.g. a PyTorch pinned
+     tensor) is adopted in place: no copy and no new pin; *granted_out gets WSR_REG_PREPINNED.
+   - Any other range is pinned with hipHostRegister only if `flags` has WSR_REG_PIN; with
+     WSR_REG_READONLY as well, a read-only pin is requested first (Sec. 5.1, read-only intent) and
+     *granted_out reports WSR_REG_READONLY if it was granted.  A refused pin returns
+     WSR_E_UNSUPPORTED: registration and direct read are separate capabilities (Sec. 7.3).  Without
+     WSR_REG_PIN such a range returns WSR_E_UNSUPPORTED.  Map file pages MAP_SHARED: pinning a
+     private mapping for write would turn file pages into anonymous copies (Sec. 5.3).
+   - Synchronous; callable from any thread.  dev_out receives the device address; granted_out may
+     be NULL. */
+#define WSR_REG_READONLY 1u     /* request: read-only mapping       | granted: read-only       */
+#define WSR_REG_PIN 2u          /* request: pin a range not yet device-visible                 */
+#define WSR_REG_PREPINNED 4u    /* granted: range was already device-visible, adopted in place  */
+wsr_status wsr_register_host(const void* host, size_t bytes, unsigned flags, const void** dev_out,
+                             unsigned* granted_out);
+
+/* Release the registration made for `host` (unpins only what wsr_register_host pinned).  Call it
+   after the last kernel reading the range has completed and before unmapping the range (Alg. 1's
+   deleter order: release the GPU view, then unmap).  WSR_E_STATE if `host` is not registered. */
+wsr_status wsr_unregister_host(const void* host);
+
+/* ---- streaming-read probe --------------------------------------------------------------------
+
+   *sum_dev = sum over i < n of buf[i], accumulated in fp64: the pure-read reference that streams
+   every byte once with no other arithmetic (Sec. 3.1, Sec. 3.3).  Per-block fp64 partial sums
+   are combined in a fixed order on the device; the result stays in device memory.
+   buf: fp32, 16-byte aligned, device-visible; n >= 0 (n = 0 gives 0).  sum_dev: one fp64,
+   device memory.  ws: at least wsr_probe_workspace_bytes(n) bytes of device memory, 16-byte
+   aligned, ZERO-FILLED BEFORE ITS FIRST USE; every completed call leaves it ready for the next. */
+size_t wsr_probe_workspace_bytes(size_t n);
+wsr_status wsr_probe_read(const float* buf, size_t n, double* sum_dev, void* ws, size_t ws_bytes,
+                          void* stream);
+
+/* ---- single-token GEMVs (Sec. 3.1: one token, one weight read per byte) ------------------------
+
+   wsr_gemv_f16: y[i] = sum_k W[i*K + k] * x[k] for i < M, with W and x both fp16 (fmt WSR_F16) or
+   both bf16 (WSR_BF16), products and sums in fp32, y fp32.
+   W: (M, K) row-major, 16-byte aligned; x: K elements, 16-byte aligned; y: M floats, 4-byte
+   aligned.  M >= 0, K >= 0, K % 8 == 0 (K = 0 gives y = 0). */
+wsr_status wsr_gemv_f16(const void* W, const void* x, float* y, int64_t M, int64_t K, int fmt,
+                        void* stream);
+
+/* wsr_gemv_q4: y[i] = sum_k w[i,k] * x[k] with w[i,k] = q[i,k] * s[i, k/32].
+   Wq: uint8 (M, K/2), byte j of row i holds q[i,2j] in its low nibble and q[i,2j+1] in its high
+   nibble, two's-complement int4 in -8..7; 16-byte aligned.  scales: fp16 bits (M, K/32), 2-byte
+   aligned.  x: fp16[K], 16-byte aligned.  y: fp32[M].  K % 32 == 0.  Dequantised weights are
+   exact (q * s needs 15 significant bits) and every product and sum is fp32. */
+wsr_status wsr_gemv_q4(const uint8_t* Wq, const uint16_t* scales, const uint16_t* x, float* y,
+                       int64_t M, int64_t K, void* stream);
+
+/* ---- decode weight sweep ----------------------------------------------------------------------
+
+   For t in [0, n_tokens), for m in [0, n) in order: y_m(t) = W_m . x_m(t), where
+   x_m(t) = x + t * x_tok_stride bytes and y_m(t) = y + t * y_tok_stride bytes.  One batch-1 token
+   reads every matrix once (Sec. 6.2) and a pass over all of them is ordered on the GPU with no
+   host synchronisation (Sec. 3.1; C3 of Table 1).  Each matrix follows wsr_gemv_f16 (fmt WSR_F16
+   or WSR_BF16) or wsr_gemv_q4 (WSR_Q4, `scales` set) and their layout and alignment rules.
+   Matrices of one token run in one persistent launch unless a matrix has WSR_MAT_AFTER_PREVIOUS,
+   which starts a new launch so that it may read outputs of earlier matrices of the same token.
+   ws: at least wsr_sweep_workspace_bytes(mats, n) bytes of device memory, 256-byte aligned. */
+#define WSR_MAT_AFTER_PREVIOUS 1
+typedef struct wsr_mat {
+    int32_t fmt;            /* wsr_fmt                                                    */
+    int32_t flags;          /* 0 or WSR_MAT_AFTER_PREVIOUS                                */
+    int64_t M, K;
+    const void* w;          /* weights (16-bit) or packed int4 codes (q4)                  */
+    const void* scales;     /* q4 block scales, NULL otherwise                            */
+    const void* x;          /* activation of token 0                                      */
+    int64_t x_tok_stride;   /* bytes between tokens' activations (0: same x every token)  */
+    float* y;               /* output of token 0                                          */
+    int64_t y_tok_stride;   /* bytes between tokens' outputs                              */
+} wsr_mat;
+
+size_t wsr_sweep_workspace_bytes(const wsr_mat* mats, int32_t n);
+wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, void* ws,
+                            size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* WSR_H */

@@ -1,0 +1,268 @@
+/*
+ * wsr_api.cpp - the C ABI of libwsr (declared in include/wsr.h): argument checks, error reporting,
+ * the host-range registry and launch orchestration.  Every check runs before anything is enqueued,
+ * so a rejected call leaves the stream untouched.  Argument checks make no HIP call.
+ */
+#include <hip/hip_runtime_api.h>
+#include <unistd.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <map>
+#include <mutex>
+#include <vector>
+
+#include "wsr.h"
+#include "wsr_internal.h"
+
+using wsr::DevMat;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+wsr_status fail(wsr_status st, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+wsr_status ok() {
+    g_err[0] = '\0';
+    return WSR_OK;
+}
+
+wsr_status hip_fail(hipError_t e, const char* what) {
+    return fail(WSR_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+/* a * b * c without overflow of int64 (all arguments >= 0). */
+bool mul_fits(int64_t a, int64_t b, int64_t c = 1) {
+    const __int128 r = (__int128)a * b * c;
+    return r <= INT64_MAX;
+}
+
+struct Reg {
+    size_t bytes;
+    void* dev;
+    bool pinned_here;
+};
+std::mutex g_mu;
+std::map<uintptr_t, Reg> g_reg;
+
+/* Shared validation of one matrix (standalone GEMV or sweep entry). */
+wsr_status check_matrix(int fmt, int64_t M, int64_t K, const void* w, const void* scales,
+                        const void* x, const float* y, const char* who) {
+    if (fmt != WSR_F16 && fmt != WSR_BF16 && fmt != WSR_Q4)
+        return fail(WSR_E_ARG, "%s: unknown format %d", who, fmt);
+    if (M < 0 || K < 0) return fail(WSR_E_ARG, "%s: negative size M=%lld K=%lld", who, (long long)M, (long long)K);
+    if (!mul_fits(M, K, 2)) return fail(WSR_E_SIZE, "%s: M*K overflows", who);
+    if (fmt == WSR_Q4 ? (K % 32 != 0) : (K % 8 != 0))
+        return fail(WSR_E_ALIGN, "%s: K=%lld must be a multiple of %d", who, (long long)K, fmt == WSR_Q4 ? 32 : 8);
+    if (M == 0) return WSR_OK;
+    if (!w || !x || !y) return fail(WSR_E_ARG, "%s: null weight, activation or output pointer", who);
+    if (fmt == WSR_Q4 && !scales) return fail(WSR_E_ARG, "%s: q4 needs scales", who);
+    if (!aligned(w, 16) || !aligned(x, 16))
+        return fail(WSR_E_ALIGN, "%s: weights and activations must be 16-byte aligned", who);
+    if (!aligned(y, 4)) return fail(WSR_E_ALIGN, "%s: output must be 4-byte aligned", who);
+    if (fmt == WSR_Q4 && !aligned(scales, 2)) return fail(WSR_E_ALIGN, "%s: scales must be 2-byte aligned", who);
+    return WSR_OK;
+}
+
+DevMat make_devmat(int fmt, int64_t M, int64_t K, const void* w, const void* scales, const void* x,
+                   float* y) {
+    DevMat d{};
+    d.w = w;
+    d.s = fmt == WSR_Q4 ? scales : nullptr;
+    d.x = x;
+    d.y = y;
+    d.M = M;
+    d.fmt = fmt;
+    if (fmt == WSR_Q4) {
+        d.nc = K / 32;
+        d.row_bytes = K / 2 + (K / 32) * 2;
+    } else {
+        d.nc = K / 8;
+        d.row_bytes = K * 2;
+    }
+    if (d.row_bytes == 0) d.row_bytes = 1;   /* K = 0: rows still need an owner to write y = 0 */
+    return d;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* wsr_last_error(void) { return g_err; }
+
+int wsr_abi_version(void) { return WSR_ABI_VERSION; }
+
+/* ---------------------------------- host ranges -------------------------------------------- */
+
+wsr_status wsr_register_host(const void* host, size_t bytes, unsigned flags, const void** dev_out,
+                             unsigned* granted_out) {
+    if (!host || !dev_out) return fail(WSR_E_ARG, "register_host: null pointer");
+    if (bytes == 0) return fail(WSR_E_ARG, "register_host: empty range");
+    if (flags & ~(WSR_REG_READONLY | WSR_REG_PIN)) return fail(WSR_E_ARG, "register_host: unknown flags %#x", flags);
+    const long page = sysconf(_SC_PAGESIZE);
+    if (!aligned(host, (uintptr_t)page) || bytes % (size_t)page != 0)
+        return fail(WSR_E_ALIGN, "register_host: base %p and length %zu must be multiples of the page size %ld",
+                    host, bytes, page);
+    std::lock_guard<std::mutex> lk(g_mu);
+    const uintptr_t key = reinterpret_cast<uintptr_t>(host);
+    if (g_reg.count(key)) return fail(WSR_E_STATE, "register_host: %p is already registered", host);
+
+    unsigned granted = 0;
+    void* dev = nullptr;
+    bool pinned_here = false;
+    hipPointerAttribute_t attr{};
+    const hipError_t qa = hipPointerGetAttributes(&attr, host);
+    if (qa == hipSuccess && attr.type == hipMemoryTypeHost && attr.devicePointer != nullptr) {
+        dev = attr.devicePointer;               /* already pinned and mapped: adopt in place */
+        granted |= WSR_REG_PREPINNED;
+    } else {
+        (void)hipGetLastError();                /* an unknown pointer is not an error here */
+        if (!(flags & WSR_REG_PIN))
+            return fail(WSR_E_UNSUPPORTED,
+                        "register_host: %p is not device-visible host memory (pass WSR_REG_PIN to pin it)", host);
+        void* h = const_cast<void*>(host);
+        hipError_t e = hipErrorNotSupported;
+        if (flags & WSR_REG_READONLY) {
+            e = hipHostRegister(h, bytes, hipHostRegisterMapped | hipHostRegisterReadOnly);
+            if (e == hipSuccess) granted |= WSR_REG_READONLY;
+            else (void)hipGetLastError();
+        }
+        if (e != hipSuccess) e = hipHostRegister(h, bytes, hipHostRegisterMapped);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(WSR_E_UNSUPPORTED, "register_host: the runtime refused to pin %p (+%zu): %s", host,
+                        bytes, hipGetErrorString(e));
+        }
+        pinned_here = true;
+        e = hipHostGetDevicePointer(&dev, h, 0);
+        if (e != hipSuccess) {
+            (void)hipHostUnregister(h);
+            return hip_fail(e, "register_host: hipHostGetDevicePointer");
+        }
+    }
+    g_reg[key] = Reg{bytes, dev, pinned_here};
+    *dev_out = dev;
+    if (granted_out) *granted_out = granted;
+    return ok();
+}
+
+wsr_status wsr_unregister_host(const void* host) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_reg.find(reinterpret_cast<uintptr_t>(host));
+    if (it == g_reg.end()) return fail(WSR_E_STATE, "unregister_host: %p is not registered", host);
+    if (it->second.pinned_here) {
+        const hipError_t e = hipHostUnregister(const_cast<void*>(host));
+        if (e != hipSuccess) return hip_fail(e, "unregister_host: hipHostUnregister");
+    }
+    g_reg.erase(it);
+    return ok();
+}
+
+/* ---------------------------------- probe --------------------------------------------------- */
+
+size_t wsr_probe_workspace_bytes(size_t n) {
+    return 64 + 8 * (size_t)wsr::probe_grid((int64_t)n);
+}
+
+wsr_status wsr_probe_read(const float* buf, size_t n, double* sum_dev, void* ws, size_t ws_bytes,
+                          void* stream) {
+    if (n > (size_t)INT64_MAX / 4) return fail(WSR_E_SIZE, "probe_read: n too large");
+    if ((n && !buf) || !sum_dev || !ws) return fail(WSR_E_ARG, "probe_read: null pointer");
+    if (!aligned(buf, 16) || !aligned(ws, 16) || !aligned(sum_dev, 8))
+        return fail(WSR_E_ALIGN, "probe_read: buf and ws must be 16-byte and sum_dev 8-byte aligned");
+    const size_t need = wsr_probe_workspace_bytes(n);
+    if (ws_bytes < need) return fail(WSR_E_SIZE, "probe_read: workspace %zu < %zu bytes", ws_bytes, need);
+    const hipError_t e = wsr::launch_probe(buf, (int64_t)n, sum_dev, ws, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "probe_read: launch");
+    return ok();
+}
+
+/* ---------------------------------- GEMVs --------------------------------------------------- */
+
+wsr_status wsr_gemv_f16(const void* W, const void* x, float* y, int64_t M, int64_t K, int fmt,
+                        void* stream) {
+    if (fmt != WSR_F16 && fmt != WSR_BF16) return fail(WSR_E_ARG, "gemv_f16: format must be WSR_F16 or WSR_BF16");
+    wsr_status st = check_matrix(fmt, M, K, W, nullptr, x, y, "gemv_f16");
+    if (st != WSR_OK) return st;
+    if (M == 0) return ok();
+    const hipError_t e = wsr::launch_gemv(make_devmat(fmt, M, K, W, nullptr, x, y), static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "gemv_f16: launch");
+    return ok();
+}
+
+wsr_status wsr_gemv_q4(const uint8_t* Wq, const uint16_t* scales, const uint16_t* x, float* y,
+                       int64_t M, int64_t K, void* stream) {
+    wsr_status st = check_matrix(WSR_Q4, M, K, Wq, scales, x, y, "gemv_q4");
+    if (st != WSR_OK) return st;
+    if (M == 0) return ok();
+    const hipError_t e = wsr::launch_gemv(make_devmat(WSR_Q4, M, K, Wq, scales, x, y), static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "gemv_q4: launch");
+    return ok();
+}
+
+/* ---------------------------------- decode sweep -------------------------------------------- */
+
+size_t wsr_sweep_workspace_bytes(const wsr_mat* mats, int32_t n) {
+    (void)mats;
+    if (n <= 0) return 0;
+    return ((size_t)n * sizeof(DevMat) + 255) / 256 * 256;
+}
+
+wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, void* ws,
+                            size_t ws_bytes, void* stream) {
+    if (n < 0 || n_tokens < 1) return fail(WSR_E_ARG, "decode_sweep: n=%d n_tokens=%d", n, n_tokens);
+    if (n == 0) return ok();
+    if (!mats || !ws) return fail(WSR_E_ARG, "decode_sweep: null pointer");
+    if (!aligned(ws, 256)) return fail(WSR_E_ALIGN, "decode_sweep: workspace must be 256-byte aligned");
+    const size_t need = wsr_sweep_workspace_bytes(mats, n);
+    if (ws_bytes < need) return fail(WSR_E_SIZE, "decode_sweep: workspace %zu < %zu bytes", ws_bytes, need);
+
+    std::vector<DevMat> tab((size_t)n);
+    struct Seg { int first, count, fmt; int64_t total; };
+    std::vector<Seg> segs;
+    char who[64];
+    for (int32_t i = 0; i < n; ++i) {
+        const wsr_mat& m = mats[i];
+        std::snprintf(who, sizeof who, "decode_sweep: matrix %d", i);
+        wsr_status st = check_matrix(m.fmt, m.M, m.K, m.w, m.scales, m.x, m.y, who);
+        if (st != WSR_OK) return st;
+        if (m.flags & ~WSR_MAT_AFTER_PREVIOUS) return fail(WSR_E_ARG, "%s: unknown flags %#x", who, m.flags);
+        if (m.x_tok_stride < 0 || m.y_tok_stride < 0 || m.x_tok_stride % 16 || m.y_tok_stride % 4)
+            return fail(WSR_E_ALIGN, "%s: token strides must be >= 0 and multiples of 16 (x) and 4 (y)", who);
+        if (!mul_fits(m.x_tok_stride, n_tokens) || !mul_fits(m.y_tok_stride, n_tokens))
+            return fail(WSR_E_SIZE, "%s: token strides overflow", who);
+        if (segs.empty() || (m.flags & WSR_MAT_AFTER_PREVIOUS)) segs.push_back(Seg{i, 0, m.fmt, 0});
+        Seg& g = segs.back();
+        DevMat d = make_devmat(m.fmt, m.M, m.K, m.w, m.scales, m.x, m.y);
+        d.x_stride = m.x_tok_stride;
+        d.y_stride = m.y_tok_stride;
+        d.cost0 = g.total;
+        if (!mul_fits(d.M, d.row_bytes) || g.total > INT64_MAX / 4 - d.M * d.row_bytes)
+            return fail(WSR_E_SIZE, "%s: weight stream too large", who);
+        g.total += d.M * d.row_bytes;
+        if (g.fmt != m.fmt) g.fmt = 0;
+        g.count += 1;
+        tab[(size_t)i] = d;
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    DevMat* dtab = static_cast<DevMat*>(ws);
+    hipError_t e = wsr::launch_put_table(dtab, tab.data(), n, s);
+    if (e != hipSuccess) return hip_fail(e, "decode_sweep: table upload");
+    for (int32_t t = 0; t < n_tokens; ++t)
+        for (const Seg& g : segs) {
+            e = wsr::launch_sweep(dtab + g.first, g.count, g.total, g.fmt, t, s);
+            if (e != hipSuccess) return hip_fail(e, "decode_sweep: launch");
+        }
+    return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,44 @@
+/*
+ * wsr_internal.h - what the host side of libwsr passes to the kernels.
+ *
+ * A matrix as the kernels see it (built by the host from a wsr_mat or a GEMV call).  Costs are in
+ * bytes of weight stream (weights plus scales), the unit the work is balanced on.
+ */
+#ifndef WSR_INTERNAL_H
+#define WSR_INTERNAL_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+namespace wsr {
+
+enum : int32_t { FMT_F16 = 1, FMT_BF16 = 2, FMT_Q4 = 3 };
+
+struct alignas(16) DevMat {
+    const void* w;          /* 16-bit weights or packed int4 codes                         */
+    const void* s;          /* q4 block scales                                              */
+    const void* x;          /* activation of token 0                                        */
+    float* y;               /* output of token 0                                            */
+    int64_t M;              /* rows                                                         */
+    int64_t nc;             /* per row: 16-byte weight chunks (16-bit) or 32-weight blocks  */
+    int64_t x_stride;       /* bytes between tokens                                         */
+    int64_t y_stride;
+    int64_t cost0;          /* weight-stream byte offset of row 0 within its launch         */
+    int64_t row_bytes;      /* weight-stream bytes per row                                  */
+    int32_t fmt;
+    int32_t pad_[3];
+};
+static_assert(sizeof(DevMat) == 96, "DevMat layout");
+
+/* Launchers (defined with the kernels).  All return the status of the launch. */
+hipError_t launch_probe(const float* buf, int64_t n, double* sum_dev, void* ws, hipStream_t s);
+int64_t probe_grid(int64_t n);
+
+hipError_t launch_gemv(const DevMat& m, hipStream_t s);
+hipError_t launch_put_table(DevMat* dst, const DevMat* src, int n, hipStream_t s);
+hipError_t launch_sweep(const DevMat* tab, int nmat, int64_t total_bytes, int fmt_all,
+                        int32_t token, hipStream_t s);
+
+}  // namespace wsr
+
+#endif

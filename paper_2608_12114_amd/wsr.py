@@ -1,0 +1,150 @@
+"""Python binding of libwsr: the entry points of include/wsr.h under the same names.
+
+Argument marshalling only: every operation runs in the HIP kernels of libwsr.so, and importing this
+module fails loudly when the library is not built.  Pointers are plain integers or objects with a
+`data_ptr()` method (PyTorch tensors); `stream` is a hipStream_t as an integer, an object with a
+`cuda_stream` attribute (a torch.cuda.Stream), or None for the null stream.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libwsr.so")
+
+WSR_OK, WSR_E_ARG, WSR_E_ALIGN, WSR_E_SIZE, WSR_E_UNSUPPORTED, WSR_E_STATE, WSR_E_HIP = range(7)
+STATUS_NAMES = {0: "WSR_OK", 1: "WSR_E_ARG", 2: "WSR_E_ALIGN", 3: "WSR_E_SIZE",
+                4: "WSR_E_UNSUPPORTED", 5: "WSR_E_STATE", 6: "WSR_E_HIP"}
+WSR_F16, WSR_BF16, WSR_Q4 = 1, 2, 3
+WSR_REG_READONLY, WSR_REG_PIN, WSR_REG_PREPINNED = 1, 2, 4
+WSR_MAT_AFTER_PREVIOUS = 1
+
+
+class WsrError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+class wsr_mat(ctypes.Structure):
+    _fields_ = [("fmt", ctypes.c_int32), ("flags", ctypes.c_int32),
+                ("M", ctypes.c_int64), ("K", ctypes.c_int64),
+                ("w", ctypes.c_void_p), ("scales", ctypes.c_void_p),
+                ("x", ctypes.c_void_p), ("x_tok_stride", ctypes.c_int64),
+                ("y", ctypes.c_void_p), ("y_tok_stride", ctypes.c_int64)]
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built: run `python -c 'import __graft_entry__ as g; g.build()'` "
+                      "from the repository root")
+
+# PyTorch ships its own HIP runtime.  Loading it first makes libwsr.so bind to that same runtime
+# (its libamdhip64.so.7 dependency is then already satisfied); loading libwsr.so first would put a
+# second HIP/HSA runtime into the process, and whichever initialises second finds no device.
+import torch  # noqa: E402,F401
+
+_L = ctypes.CDLL(LIB_PATH)
+_vp, _sz, _i64, _i32, _u = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint
+_L.wsr_last_error.restype = ctypes.c_char_p
+_L.wsr_last_error.argtypes = []
+_L.wsr_abi_version.restype = ctypes.c_int
+_L.wsr_abi_version.argtypes = []
+_L.wsr_register_host.argtypes = [_vp, _sz, _u, ctypes.POINTER(_vp), ctypes.POINTER(_u)]
+_L.wsr_unregister_host.argtypes = [_vp]
+_L.wsr_probe_workspace_bytes.argtypes = [_sz]
+_L.wsr_probe_workspace_bytes.restype = _sz
+_L.wsr_probe_read.argtypes = [_vp, _sz, _vp, _vp, _sz, _vp]
+_L.wsr_gemv_f16.argtypes = [_vp, _vp, _vp, _i64, _i64, ctypes.c_int, _vp]
+_L.wsr_gemv_q4.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _vp]
+_L.wsr_sweep_workspace_bytes.argtypes = [ctypes.POINTER(wsr_mat), _i32]
+_L.wsr_sweep_workspace_bytes.restype = _sz
+_L.wsr_decode_sweep.argtypes = [ctypes.POINTER(wsr_mat), _i32, _i32, _vp, _sz, _vp]
+for _f in ("wsr_register_host", "wsr_unregister_host", "wsr_probe_read", "wsr_gemv_f16",
+           "wsr_gemv_q4", "wsr_decode_sweep"):
+    getattr(_L, _f).restype = ctypes.c_int
+
+
+def lib() -> ctypes.CDLL:
+    return _L
+
+
+def _ptr(a) -> int | None:
+    if a is None:
+        return None
+    if hasattr(a, "data_ptr"):
+        return a.data_ptr()
+    return int(a)
+
+
+def _stream(s) -> int | None:
+    if s is None:
+        return None
+    if hasattr(s, "cuda_stream"):
+        return s.cuda_stream
+    return int(s)
+
+
+def _check(st: int) -> None:
+    if st != WSR_OK:
+        raise WsrError(st, wsr_last_error())
+
+
+def wsr_last_error() -> str:
+    return _L.wsr_last_error().decode()
+
+
+def wsr_abi_version() -> int:
+    return _L.wsr_abi_version()
+
+
+def wsr_register_host(host, nbytes: int, flags: int = 0) -> tuple[int, int]:
+    """Returns (device address, granted flags)."""
+    dev, granted = _vp(), _u()
+    _check(_L.wsr_register_host(_ptr(host), nbytes, flags, ctypes.byref(dev), ctypes.byref(granted)))
+    return dev.value, granted.value
+
+
+def wsr_unregister_host(host) -> None:
+    _check(_L.wsr_unregister_host(_ptr(host)))
+
+
+def wsr_probe_workspace_bytes(n: int) -> int:
+    return _L.wsr_probe_workspace_bytes(n)
+
+
+def wsr_probe_read(buf, n: int, sum_dev, ws, ws_bytes: int, stream=None) -> None:
+    _check(_L.wsr_probe_read(_ptr(buf), n, _ptr(sum_dev), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def wsr_gemv_f16(W, x, y, M: int, K: int, fmt: int, stream=None) -> None:
+    _check(_L.wsr_gemv_f16(_ptr(W), _ptr(x), _ptr(y), M, K, fmt, _stream(stream)))
+
+
+def wsr_gemv_q4(Wq, scales, x, y, M: int, K: int, stream=None) -> None:
+    _check(_L.wsr_gemv_q4(_ptr(Wq), _ptr(scales), _ptr(x), _ptr(y), M, K, _stream(stream)))
+
+
+def make_mats(specs) -> ctypes.Array:
+    """specs: iterable of dicts with keys fmt, M, K, w, x, y and optionally scales, flags,
+    x_tok_stride, y_tok_stride (pointers as ints or tensors)."""
+    specs = list(specs)
+    arr = (wsr_mat * max(1, len(specs)))()
+    for i, s in enumerate(specs):
+        arr[i] = wsr_mat(s["fmt"], s.get("flags", 0), s["M"], s["K"], _ptr(s["w"]),
+                         _ptr(s.get("scales")), _ptr(s["x"]), s.get("x_tok_stride", 0),
+                         _ptr(s["y"]), s.get("y_tok_stride", 0))
+    arr._n = len(specs)
+    return arr
+
+
+def _n(mats) -> int:
+    return getattr(mats, "_n", len(mats))
+
+
+def wsr_sweep_workspace_bytes(mats) -> int:
+    return _L.wsr_sweep_workspace_bytes(mats, _n(mats))
+
+
+def wsr_decode_sweep(mats, n_tokens: int, ws, ws_bytes: int, stream=None) -> None:
+    _check(_L.wsr_decode_sweep(mats, _n(mats), n_tokens, _ptr(ws), ws_bytes, _stream(stream)))

@@ -26,12 +26,23 @@ F16, BF16 = 1, 2
 _FMT = {"f16": F16, "bf16": BF16, F16: F16, BF16: BF16}
 
 
+DEV_LIB_PATH = os.path.join(_HERE, "libsynth_dev.so")
+DEV_SRC_PATH = os.path.join(_HERE, "synth_dev.hip")
+
+
 def build() -> str:
-    """Compile libsynth.so (host only)."""
+    """Compile libsynth.so (host) and libsynth_dev.so (the same generator for gfx950)."""
     cmd = ["gcc", "-O2", "-ffp-contract=off", "-fPIC", "-shared", "-fopenmp",
            SRC_PATH, "-o", LIB_PATH + ".tmp", "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(LIB_PATH + ".tmp", LIB_PATH)
+    cmd = ["hipcc", "-O3", "-fPIC", "-shared", "--offload-arch=gfx950", "-ffp-contract=off",
+           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           DEV_SRC_PATH, "-o", DEV_LIB_PATH + ".tmp"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"building {DEV_SRC_PATH} failed:\n{r.stderr}")
+    os.replace(DEV_LIB_PATH + ".tmp", DEV_LIB_PATH)
     return LIB_PATH
 
 
@@ -52,19 +63,22 @@ def lib() -> ctypes.CDLL:
         L.synth_enc_f16.restype = ctypes.c_uint16
         L.synth_enc_bf16.argtypes = [dbl]
         L.synth_enc_bf16.restype = ctypes.c_uint16
-        L.synth_normal.argtypes = [u64, u64, u64]
-        L.synth_normal.restype = dbl
         L.synth_grid.argtypes = [u64, u64, u64]
         L.synth_grid.restype = ctypes.c_float
         L.synth_int4.argtypes = [u64, u64, u64]
         L.synth_int4.restype = i32
-        L.synth_normal_f64.argtypes = [vp, i64, u64, u64, u64, i32]
-        L.synth_normal16.argtypes = [vp, i64, u64, u64, u64, dbl, i32, i32]
+        L.synth_table_bytes.argtypes = []
+        L.synth_table_bytes.restype = ctypes.c_size_t
+        L.synth_table_build.argtypes = [vp, i32, dbl]
+        L.synth_table_build.restype = i32
+        L.synth_normal16.argtypes = [vp, i64, u64, u64, u64, vp, i32]
+        L.synth_normal16_one.argtypes = [vp, u64, u64, u64]
+        L.synth_normal16_one.restype = ctypes.c_uint16
         L.synth_grid_f32.argtypes = [vp, i64, u64, u64, u64, i32]
         L.synth_q4.argtypes = [vp, i64, u64, u64, u64, i32]
         L.synth_uniform16.argtypes = [vp, i64, u64, u64, u64, dbl, dbl, i32, i32]
         L.synth_encode16.argtypes = [vp, vp, i64, i32]
-        for f in ("synth_normal_f64", "synth_normal16", "synth_grid_f32", "synth_q4",
+        for f in ("synth_normal16", "synth_grid_f32", "synth_q4",
                   "synth_uniform16", "synth_encode16"):
             getattr(L, f).restype = None
         _lib = L
@@ -86,17 +100,31 @@ def _out(out, shape, dtype):
     return out
 
 
+_tables = {}
+
+
+def table(fmt, sigma) -> np.ndarray:
+    """Sampling table of RNE(sigma * N(0, 1)) in fp16/bf16 (raw bytes of the C struct, cached)."""
+    key = (_FMT[fmt], float(sigma))
+    if key not in _tables:
+        t = np.zeros(lib().synth_table_bytes(), dtype=np.uint8)
+        if lib().synth_table_build(t.ctypes.data, key[0], key[1]) != 0:
+            raise ValueError(f"cannot build a sampling table for sigma={sigma}")
+        _tables[key] = t
+    return _tables[key]
+
+
+def table_arrays(fmt, sigma):
+    """(accept thresholds uint64[65536], alias codes uint16[65536]) of the sampling table."""
+    t = table(fmt, sigma)
+    return t[: 8 * 65536].view(np.uint64), t[8 * 65536: 8 * 65536 + 2 * 65536].view(np.uint16)
+
+
 def normal16(shape, sigma, fmt, seed=0, stream=0, e0=0, out=None, threads=None):
-    """sigma * N(0,1) rounded to fp16/bf16 bits; flat element e0 + i of the stream."""
+    """Codes of RNE(sigma * N(0,1)) in fp16/bf16 (uint16); flat element e0 + i of the stream."""
     a = _out(out, shape, np.uint16)
-    lib().synth_normal16(a.ctypes.data, a.size, seed, stream, e0, float(sigma), _FMT[fmt],
+    lib().synth_normal16(a.ctypes.data, a.size, seed, stream, e0, table(fmt, sigma).ctypes.data,
                          threads or default_threads())
-    return a
-
-
-def normal_f64(n, seed=0, stream=0, e0=0, threads=None):
-    a = np.empty(n, dtype=np.float64)
-    lib().synth_normal_f64(a.ctypes.data, n, seed, stream, e0, threads or default_threads())
     return a
 
 

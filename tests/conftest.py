@@ -1,6 +1,8 @@
 import os
 import sys
 
+import torch  # noqa: F401  (before any HIP library: one HIP runtime per process, PyTorch's)
+
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)

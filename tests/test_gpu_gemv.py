@@ -1,0 +1,148 @@
+"""16-bit and q4 GEMVs on the GPU against the oracle: relative L2 error within 2e-3 (fp32
+accumulation), and exact results where the method reaches an exact value (unit vectors, identity)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from synth import device as dv
+from synth import workloads as wl
+from gpu_util import TOL, f32_bits, needs_gpu, rel_l2, sample_rows, stream
+
+from paper_2608_12114_amd import wsr
+
+pytestmark = [pytest.mark.gpu, needs_gpu]
+FMT = {"f16": wsr.WSR_F16, "bf16": wsr.WSR_BF16}
+
+
+def gemv16(W, x, fmt, M, K):
+    y = torch.full((max(M, 1),), float("nan"), dtype=torch.float32, device="cuda")
+    wsr.wsr_gemv_f16(dv.to_device(W), dv.to_device(x), y, M, K, FMT[fmt], stream())
+    return y[:M].cpu().numpy()
+
+
+def gemvq4(Wq, S, x, M, K):
+    y = torch.full((max(M, 1),), float("nan"), dtype=torch.float32, device="cuda")
+    wsr.wsr_gemv_q4(dv.to_device(Wq), dv.to_device(S), dv.to_device(x), y, M, K, stream())
+    return y[:M].cpu().numpy()
+
+
+def dec(codes, fmt):
+    if fmt == "f16":
+        return codes.view(np.float16).astype(np.float64)
+    return (codes.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+SHAPES16 = [(1, 8), (3, 24), (37, 520), (64, 4104), (257, 4096), (4096, 4096), (1000, 14336),
+            (9000, 1024), (2, 28672)]
+
+
+@pytest.mark.parametrize("fmt", ["f16", "bf16"])
+@pytest.mark.parametrize("M,K", SHAPES16)
+def test_gemv16_parity(fmt, M, K):
+    W = synth.normal16((M, K), wl.W_SIGMA, fmt, seed=0, stream=101)
+    x = synth.normal16(K, wl.X_SIGMA, fmt, seed=0, stream=102)
+    y = gemv16(W, x, fmt, M, K)
+    yo = oracle.get().gemv16(W, x, fmt, threads=8)
+    assert rel_l2(y, yo) <= TOL
+    assert np.array_equal(f32_bits(y), f32_bits(gemv16(W, x, fmt, M, K)))   # deterministic
+
+
+@pytest.mark.parametrize("fmt", ["f16", "bf16"])
+def test_gemv16_unit_vectors_exact(fmt):
+    M, K = 300, 1040
+    W = synth.normal16((M, K), wl.W_SIGMA, fmt, seed=1, stream=103)
+    if fmt == "f16":   # include subnormal weights: they must not be flushed
+        W[:5, 7] = [0x0001, 0x8003, 0x03FF, 0x0200, 0x8001]
+    one, zero = synth.encode16([1.0, 0.0], fmt)
+    for j in (0, 7, 8, 511, 512, K - 1):
+        e = np.full(K, zero, np.uint16)
+        e[j] = one
+        y = gemv16(W, e, fmt, M, K)
+        assert np.array_equal(y.astype(np.float64), dec(W[:, j], fmt)), j
+
+
+@pytest.mark.parametrize("fmt", ["f16", "bf16"])
+def test_gemv16_identity_ones_and_empty(fmt):
+    K = 512
+    one, zero = synth.encode16([1.0, 0.0], fmt)
+    eye = np.full((K, K), zero, np.uint16)
+    np.fill_diagonal(eye, one)
+    x = synth.normal16(K, 1.0, fmt, seed=2, stream=104)
+    assert np.array_equal(gemv16(eye, x, fmt, K, K).astype(np.float64), dec(x, fmt))
+    W = synth.normal16((77, K), wl.W_SIGMA, fmt, seed=2, stream=105)
+    rows = dec(W, fmt).sum(axis=1)
+    assert rel_l2(gemv16(W, np.full(K, one, np.uint16), fmt, 77, K), rows) <= TOL
+    # K = 0: every output is the empty sum
+    y = torch.full((5,), 7.0, device="cuda")
+    wsr.wsr_gemv_f16(y, y, y, 5, 0, FMT[fmt], stream())
+    assert y.cpu().tolist() == [0.0] * 5
+    # M = 0: nothing is written
+    wsr.wsr_gemv_f16(None, None, None, 0, 16, FMT[fmt], stream())
+
+
+@pytest.mark.parametrize("N", wl.SWEEP_N)
+def test_gemv_bf16_size_sweep_config(N):
+    """The bf16 size-sweep shapes: reduction 4096, N output rows (2 MiB ... 1100 MiB of weights)."""
+    K = wl.SWEEP_K
+    W = synth.normal16((N, K), wl.W_SIGMA, "bf16", seed=0, stream=1)
+    x = synth.normal16(K, wl.X_SIGMA, "bf16", seed=0, stream=2)
+    y = gemv16(W, x, "bf16", N, K)
+    rows = sample_rows(N, 256)
+    yo = oracle.get().gemv16(W[rows], x, "bf16", threads=8)
+    assert rel_l2(y[rows], yo) <= TOL
+
+
+def test_gemv_f16_config_full():
+    """fp16 4096 x 4096 GEMV, every output against the oracle."""
+    cfg = wl.GemvConfig()
+    W = synth.normal16((cfg.M, cfg.K), wl.W_SIGMA, "f16", seed=0, stream=1)
+    x = synth.normal16(cfg.K, wl.X_SIGMA, "f16", seed=0, stream=2)
+    y = gemv16(W, x, "f16", cfg.M, cfg.K)
+    assert rel_l2(y, oracle.get().gemv16(W, x, "f16", threads=8)) <= TOL
+
+
+# ---- q4 ---------------------------------------------------------------------------------------
+
+SHAPESQ4 = [(1, 32), (5, 64), (37, 2080), (300, 4096), (4096, 4096), (1024, 14336), (14336, 4096),
+            (3, 28672)]
+
+
+@pytest.mark.parametrize("M,K", SHAPESQ4)
+def test_gemv_q4_parity(M, K):
+    Wq = synth.q4_codes(M, K, seed=0, stream=201)
+    S = synth.q4_scales(M, K, seed=0, stream=202)
+    x = synth.normal16(K, wl.X_SIGMA, "f16", seed=0, stream=203)
+    y = gemvq4(Wq, S, x, M, K)
+    assert rel_l2(y, oracle.get().gemv_q4(Wq, S, x, threads=8)) <= TOL
+    assert np.array_equal(f32_bits(y), f32_bits(gemvq4(Wq, S, x, M, K)))
+
+
+def test_gemv_q4_dequant_exact_via_unit_vectors():
+    """x = e_j returns column j of the dequantised matrix, q * s, bit for bit in fp32."""
+    M, K = 257, 4160
+    Wq = synth.q4_codes(M, K, seed=3, stream=204)
+    S = synth.q4_scales(M, K, seed=3, stream=205)
+    w = oracle.get().dequant_q4(Wq, S)
+    zero, one = synth.encode16([0.0, 1.0], "f16")
+    for j in (0, 1, 2, 3, 4, 5, 6, 7, 8, 15, 31, 32, 33, 2047, 2048, 4095, 4096, K - 1):
+        e = np.full(K, zero, np.uint16)
+        e[j] = one
+        y = gemvq4(Wq, S, e, M, K)
+        assert np.array_equal(f32_bits(y), f32_bits(w[:, j])), j
+
+
+def test_gemv_q4_identity_blocks():
+    """q = 1 on the diagonal, s = 1: y = x.  The decode sums activations with a small fixed offset
+    (8 times their block sum, removed afterwards), so this is checked to a tolerance 100 times
+    tighter than the parity bound rather than bit for bit; the bit-exact dequantisation check is
+    the unit-vector test above."""
+    K = 128
+    one = synth.encode16([1.0], "f16")[0]
+    Wq = np.zeros((K, K // 2), np.uint8)
+    for i in range(K):
+        Wq[i, i // 2] = 0x01 if i % 2 == 0 else 0x10
+    S = np.full((K, K // 32), one, np.uint16)
+    x = synth.normal16(K, 1.0, "f16", seed=4, stream=206)
+    assert rel_l2(gemvq4(Wq, S, x, K, K), x.view(np.float16).astype(np.float64)) <= TOL / 100

@@ -1,0 +1,97 @@
+"""Decode weight sweep on the GPU against the oracle, plus its structural properties: the fused,
+chained and per-matrix paths give bitwise-identical outputs, and every token reads its own
+activation and writes its own outputs."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from synth import device as dv
+from synth import workloads as wl
+from gpu_util import TOL, f32_bits, needs_gpu, rel_l2, stream, zeros_u8
+
+from paper_2608_12114_amd import wsr
+
+pytestmark = [pytest.mark.gpu, needs_gpu]
+
+
+def run_sweep(inp, tokens, chained=False):
+    for y in inp.y:
+        y.fill_(float("nan"))
+    mats = wsr.make_mats(inp.specs(chained=chained))
+    ws = zeros_u8(wsr.wsr_sweep_workspace_bytes(mats))
+    wsr.wsr_decode_sweep(mats, tokens, ws, ws.numel(), stream())
+    torch.cuda.synchronize()
+    return [y.cpu().numpy().copy() for y in inp.y]
+
+
+def oracle_y(inp, i, t, rows=None):
+    ora = oracle.get()
+    fmt = inp.fmts[i]
+    x = inp.host_x(i, t)
+    if rows is None:
+        hw = inp.host_weights(i)
+        return ora.gemv_q4(*hw, x, threads=8) if fmt == wl.Q4 else ora.gemv16(hw, x, fmt, threads=8)
+    out = []
+    for r in rows:
+        hw = inp.host_weights(i, int(r), 1)
+        out.append((ora.gemv_q4(*hw, x) if fmt == wl.Q4 else ora.gemv16(hw, x, fmt))[0])
+    return np.array(out)
+
+
+@pytest.fixture(scope="module")
+def mixed():
+    mats = wl.decode_matrices(dv.small_model(layers=3, d=512, ffn=1536, vocab=4000))
+    fmts = [(wl.Q4, wl.BF16, wl.F16, wl.BF16)[m.layer] for m in mats]
+    return dv.SweepInputs(mats, fmts, tokens=3)
+
+
+def test_sweep_mixed_parity(mixed):
+    ys = run_sweep(mixed, 3)
+    for i in range(len(mixed.mats)):
+        for t in range(3):
+            assert rel_l2(ys[i][t], oracle_y(mixed, i, t)) <= TOL, (i, t)
+
+
+def test_sweep_paths_bitwise_identical(mixed):
+    fused = run_sweep(mixed, 3)
+    chained = run_sweep(mixed, 3, chained=True)
+    for a, b in zip(fused, chained):
+        assert np.array_equal(f32_bits(a), f32_bits(b))
+    # the standalone GEMVs of each matrix and token give the same bits
+    for i, (m, fmt) in enumerate(zip(mixed.mats, mixed.fmts)):
+        xt, _ = mixed.x[(m.layer, m.slot)]
+        for t in (0, 2):
+            y = torch.empty(m.M, dtype=torch.float32, device="cuda")
+            if fmt == wl.Q4:
+                wsr.wsr_gemv_q4(mixed.w[i], mixed.s[i], xt[t], y, m.M, m.K, stream())
+            else:
+                wsr.wsr_gemv_f16(mixed.w[i], xt[t], y, m.M, m.K, dv.WSR_FMT[fmt], stream())
+            assert np.array_equal(f32_bits(y.cpu().numpy()), f32_bits(fused[i][t])), (i, t)
+
+
+def test_sweep_same_activation_every_token(mixed):
+    specs = mixed.specs()
+    for s in specs:
+        s["x_tok_stride"] = 0
+    for y in mixed.y:
+        y.fill_(float("nan"))
+    mats = wsr.make_mats(specs)
+    ws = zeros_u8(wsr.wsr_sweep_workspace_bytes(mats))
+    wsr.wsr_decode_sweep(mats, 3, ws, ws.numel(), stream())
+    for y in mixed.y:
+        a = y.cpu().numpy()
+        assert np.array_equal(f32_bits(a[0]), f32_bits(a[1])) and np.array_equal(f32_bits(a[0]), f32_bits(a[2]))
+
+
+@pytest.mark.parametrize("layers,d,ffn", [(1, 64, 96), (2, 128, 4160)])
+@pytest.mark.parametrize("fmt", [wl.Q4, wl.BF16])
+def test_sweep_ragged_shapes(layers, d, ffn, fmt):
+    """Shapes whose rows do not fill whole 64-lane steps, one and several layers."""
+    mats = wl.decode_matrices(dv.small_model(layers=layers, d=d, ffn=ffn, vocab=333, n_q=2, n_kv=1,
+                                             head_dim=32 if d == 64 else 64))
+    inp = dv.SweepInputs(mats, [fmt] * len(mats), tokens=2)
+    ys = run_sweep(inp, 2)
+    for i in range(len(mats)):
+        for t in range(2):
+            assert rel_l2(ys[i][t], oracle_y(inp, i, t)) <= TOL, (i, t)

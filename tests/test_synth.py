@@ -88,12 +88,53 @@ def test_grid_values():
     assert abs(x.mean()) < 0.01
 
 
-def test_normal_distribution():
-    z = synth.normal_f64(200000, seed=0, stream=11)
-    assert abs(z.mean()) < 0.01 and abs(z.std() - 1) < 0.01
-    assert stats.kstest(z, "norm").pvalue > 1e-3
-    w = synth.normal16(200000, 0.02, "f16", seed=0, stream=11).view(np.float16).astype(np.float64)
-    assert abs(w.std() - 0.02) < 0.0005
+def _implied_probabilities(fmt, sigma):
+    q, alias = synth.table_arrays(fmt, sigma)
+    cap = float(1 << 48)
+    spill = np.bincount(alias, weights=cap - q.astype(np.float64), minlength=65536)
+    return (q.astype(np.float64) + spill) / 2.0 ** 64
+
+
+def _rounded_normal_mass(fmt, sigma):
+    """Independent: scipy's normal CDF over the interval of reals that rounds to each code."""
+    codes = np.arange(0x7C00 if fmt == "f16" else 0x7F80, dtype=np.uint32).astype(np.uint16)
+    if fmt == "f16":
+        v = codes.view(np.float16).astype(np.float64)
+    else:
+        v = (codes.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    mid = 0.5 * (v[1:] + v[:-1])
+    lo = np.concatenate([[0.0], mid]) / sigma
+    hi = np.concatenate([mid, [np.inf]]) / sigma
+    p = stats.norm.sf(lo) - stats.norm.sf(hi)
+    p[0] *= 2.0                       # +0 owns (-h, h)
+    full = np.zeros(65536)
+    full[: codes.size] = p
+    full[0x8001: 0x8000 + codes.size] = p[1:]
+    return full
+
+
+@pytest.mark.parametrize("fmt,sigma", [("f16", 1.0), ("f16", 0.02), ("bf16", 1.0), ("bf16", 0.02)])
+def test_sampling_table_matches_rounded_normal(fmt, sigma):
+    got = _implied_probabilities(fmt, sigma)
+    want = _rounded_normal_mass(fmt, sigma)
+    assert abs(got.sum() - 1.0) < 1e-12
+    assert np.all(np.abs(got - want) <= 1e-14 + 1e-6 * want)
+    assert got[0x7C00:0x8000].sum() == 0 and got[0xFC00:].sum() == 0 if fmt == "f16" else True
+
+
+def test_normal_draws_follow_the_table():
+    n = 4_000_000
+    a = synth.normal16(n, 0.02, "f16", seed=0, stream=11)
+    p = _implied_probabilities("f16", 0.02)
+    counts = np.bincount(a, minlength=65536)
+    big = p * n > 50                                   # chi-square over well-populated codes
+    chi2 = float((((counts[big] - n * p[big]) ** 2) / (n * p[big])).sum())
+    dof = int(big.sum()) - 1
+    assert stats.chi2.sf(chi2, dof) > 1e-4, (chi2, dof)
+    w = a.view(np.float16).astype(np.float64)
+    assert abs(w.mean()) < 1e-4 and abs(w.std() - 0.02) < 1e-4
+    one = synth.lib().synth_normal16_one(synth.table("f16", 0.02).ctypes.data, 0, 11, 12345)
+    assert one == a[12345]
 
 
 def test_int4_uniform():
