@@ -12,6 +12,7 @@ Also measured in the same run and reported under "rows" (same JSON line):
   llama8b_q4   decode sweep of the Llama-3-8B shape in 4-bit blocks (4.22 GB per token)
   size_sweep   bf16 GEMV with K = 4096 and N = 256 ... 140800 rows, resident and host-mapped
   bus          pinned host -> device copy rate, the ceiling of every host-mapped arm
+  copy         1 GiB elementwise read+write pass (calibrates the HBM byte counters; not default)
 
 Usage: python bench.py [--gpus 1] [--steps 16] [--warmup 2] [--rows probe,gemv_f16,...]
 """
@@ -290,6 +291,19 @@ def row_size_sweep(stream, wsr):
     return out
 
 
+def row_copy(stream):
+    """A plain elementwise pass of known size (1 GiB read, 1 GiB written): the calibration kernel
+    for the FETCH_SIZE / WRITE_SIZE hardware counters."""
+    import torch
+    n = 1 << 28
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    torch.neg(a, out=b)
+    t = median_of(lambda: torch.neg(a, out=b), 1, 5, stream)
+    log(f"copy: 1 GiB read + 1 GiB written in {t * 1e6:.1f} us -> {2 * 4 * n / t / 1e9:.1f} GB/s")
+    return {"bytes_read": 4 * n, "bytes_written": 4 * n, "us": t * 1e6, "GBps_rw": 2 * 4 * n / t / 1e9}
+
+
 def row_bus(stream):
     import torch
     n = 1 << 30
@@ -333,6 +347,8 @@ def main():
             rows[r] = row_size_sweep(stream, wsr)
         elif r == "bus":
             rows[r] = row_bus(stream)
+        elif r == "copy":
+            rows[r] = row_copy(stream)
         else:
             raise SystemExit(f"unknown row {r}")
 

@@ -96,11 +96,12 @@ wsr_status wsr_unregister_host(const void* host);
 /* ---- streaming-read probe --------------------------------------------------------------------
 
    *sum_dev = sum over i < n of buf[i], accumulated in fp64: the pure-read reference that streams
-   every byte once with no other arithmetic (Sec. 3.1, Sec. 3.3).  Per-block fp64 partial sums
-   are combined in a fixed order on the device; the result stays in device memory.
+   every byte once with no other arithmetic (Sec. 3.1, Sec. 3.3).  Each block sums a contiguous
+   part of the buffer into an fp64 partial in the workspace; a second launch adds the partials in
+   index order.  The result stays in device memory.
    buf: fp32, 16-byte aligned, device-visible; n >= 0 (n = 0 gives 0).  sum_dev: one fp64,
    device memory.  ws: at least wsr_probe_workspace_bytes(n) bytes of device memory, 16-byte
-   aligned, ZERO-FILLED BEFORE ITS FIRST USE; every completed call leaves it ready for the next. */
+   aligned (its contents need no initialisation). */
 size_t wsr_probe_workspace_bytes(size_t n);
 wsr_status wsr_probe_read(const float* buf, size_t n, double* sum_dev, void* ws, size_t ws_bytes,
                           void* stream);
@@ -131,7 +132,8 @@ wsr_status wsr_gemv_q4(const uint8_t* Wq, const uint16_t* scales, const uint16_t
    or WSR_BF16) or wsr_gemv_q4 (WSR_Q4, `scales` set) and their layout and alignment rules.
    Matrices of one token run in one persistent launch unless a matrix has WSR_MAT_AFTER_PREVIOUS,
    which starts a new launch so that it may read outputs of earlier matrices of the same token.
-   ws: at least wsr_sweep_workspace_bytes(mats, n) bytes of device memory, 256-byte aligned. */
+   ws: at least wsr_sweep_workspace_bytes(mats, n) bytes of device memory, 256-byte aligned; each
+   call writes the matrix table and the launches' work counters there (no initialisation needed). */
 #define WSR_MAT_AFTER_PREVIOUS 1
 typedef struct wsr_mat {
     int32_t fmt;            /* wsr_fmt                                                    */

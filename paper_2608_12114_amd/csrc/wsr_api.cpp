@@ -170,7 +170,7 @@ wsr_status wsr_unregister_host(const void* host) {
 /* ---------------------------------- probe --------------------------------------------------- */
 
 size_t wsr_probe_workspace_bytes(size_t n) {
-    return 64 + 8 * (size_t)wsr::probe_grid((int64_t)n);
+    return 8 * (size_t)wsr::probe_grid((int64_t)n);
 }
 
 wsr_status wsr_probe_read(const float* buf, size_t n, double* sum_dev, void* ws, size_t ws_bytes,
@@ -214,7 +214,7 @@ wsr_status wsr_gemv_q4(const uint8_t* Wq, const uint16_t* scales, const uint16_t
 size_t wsr_sweep_workspace_bytes(const wsr_mat* mats, int32_t n) {
     (void)mats;
     if (n <= 0) return 0;
-    return ((size_t)n * sizeof(DevMat) + 255) / 256 * 256;
+    return wsr::SWEEP_CTR_BYTES + ((size_t)n * sizeof(DevMat) + 255) / 256 * 256;
 }
 
 wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, void* ws,
@@ -254,12 +254,13 @@ wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, vo
         tab[(size_t)i] = d;
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    DevMat* dtab = static_cast<DevMat*>(ws);
-    hipError_t e = wsr::launch_put_table(dtab, tab.data(), n, s);
+    unsigned* ctr = static_cast<unsigned*>(ws);
+    DevMat* dtab = reinterpret_cast<DevMat*>(static_cast<char*>(ws) + wsr::SWEEP_CTR_BYTES);
+    hipError_t e = wsr::launch_put_table(dtab, tab.data(), n, ctr, s);
     if (e != hipSuccess) return hip_fail(e, "decode_sweep: table upload");
     for (int32_t t = 0; t < n_tokens; ++t)
         for (const Seg& g : segs) {
-            e = wsr::launch_sweep(dtab + g.first, g.count, g.total, g.fmt, t, s);
+            e = wsr::launch_sweep(dtab + g.first, g.count, g.total, g.fmt, t, ctr, s);
             if (e != hipSuccess) return hip_fail(e, "decode_sweep: launch");
         }
     return ok();

@@ -5,6 +5,10 @@
  * far below any matrix-core ridge, so it runs on the vector ALUs and is bound by HBM bandwidth.
  *  - A wavefront owns whole rows: its 64 lanes cover a row in 16-byte chunks, so every load
  *    instruction of the wave reads 1 KiB of one row, contiguous and aligned.
+ *  - Row indices are wave-uniform values held in scalar registers (the wave id goes through
+ *    readfirstlane), so row bases, table reads and loop control run on the scalar unit and the
+ *    vector ALUs only decode and multiply.  Pointers are global-address-space, giving plain global
+ *    loads with a scalar base and a 32-bit lane offset.
  *  - Weights are loaded non-temporally (each byte is used once); activations use the normal cache
  *    path, since every row of the matrix rereads them.
  *  - Each lane accumulates in fp32 with packed two-element dot products (v_dot2c_f32_f16 /
@@ -27,11 +31,24 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
 typedef __bf16 b2_t __attribute__((ext_vector_type(2)));
 
+/* global-address-space views of caller pointers */
+typedef __attribute__((address_space(1))) const u32x4 g_u32x4;
+typedef __attribute__((address_space(1))) const uint16_t g_u16;
+typedef __attribute__((address_space(1))) float g_f32;
+
 constexpr int WAVE = 64;
 
-__device__ __forceinline__ u32x4 load_once(const u32x4* p) { return __builtin_nontemporal_load(p); }
-__device__ __forceinline__ u32x4 load_reused(const u32x4* p) { return *p; }
+template <typename T>
+__device__ __forceinline__ T as_global(const void* p) { return (T)p; }
+
+__device__ __forceinline__ u32x4 load_once(g_u32x4* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ u32x4 load_reused(g_u32x4* p) { return *p; }
 __device__ __forceinline__ u32x4 zero4() { return u32x4{0u, 0u, 0u, 0u}; }
+
+/* The wave's index inside its block, as a uniform (scalar) value. */
+__device__ __forceinline__ int wave_in_block() {
+    return __builtin_amdgcn_readfirstlane((int)(threadIdx.x / WAVE));
+}
 
 /* acc + a.lo*b.lo + a.hi*b.hi for two packed 16-bit pairs, fp32 accumulate. */
 template <int FMT>
@@ -100,64 +117,67 @@ __device__ __forceinline__ double wave_sum(double v) {
 
 /* ---- 16-bit rows -------------------------------------------------------------------------------
 
-   Rows [r0, r1) of matrix d at token `token`, R rows per pass over K.  A pass over K moves in steps
-   of U chunks per lane (U * 64 chunks = U KiB per row per step); only a ragged last step masks its
-   lanes.  Lane l accumulates chunks l, l + 64, l + 128, ... of each row in that order. */
+   Rows [i, i + R) of matrix d (i wave-uniform, all R rows valid).  A pass over K moves in steps of
+   U chunks per lane (U * 64 chunks = U KiB per row per step); only a ragged last step masks its
+   lanes.  Lane l accumulates chunks l, l + 64, l + 128, ... of each row in that order, whatever R
+   and U are, so every row's result is independent of how rows were grouped. */
+template <int FMT, int R, int U>
+__device__ __forceinline__ void group16(const char* W, g_u32x4* x, g_f32* y, int64_t nc, int64_t i,
+                                        int lane) {
+    constexpr int STEP = WAVE * U;
+    float acc[R];
+    g_u32x4* wr[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        acc[r] = 0.f;
+        wr[r] = as_global<g_u32x4*>(W + (i + r) * nc * 16);
+    }
+    int64_t c0 = 0;
+    for (; c0 + STEP <= nc; c0 += STEP) {
+        u32x4 xv[U], wv[R][U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) xv[u] = load_reused(x + c0 + u * WAVE + lane);
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int u = 0; u < U; ++u) wv[r][u] = load_once(wr[r] + c0 + u * WAVE + lane);
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int u = 0; u < U; ++u) acc[r] = dot8<FMT>(wv[r][u], xv[u], acc[r]);
+    }
+    if (c0 < nc) {  /* ragged last step */
+        u32x4 xv[U], wv[R][U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t c = c0 + u * WAVE + lane;
+            xv[u] = c < nc ? load_reused(x + c) : zero4();
+#pragma unroll
+            for (int r = 0; r < R; ++r) wv[r][u] = c < nc ? load_once(wr[r] + c) : zero4();
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int u = 0; u < U; ++u) acc[r] = dot8<FMT>(wv[r][u], xv[u], acc[r]);
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const float s = wave_sum(acc[r]);
+        if (lane == 0) y[i + r] = s;
+    }
+}
+
+/* Rows [r0, r1) of matrix d at token `token` (r0, r1 wave-uniform): groups of R rows, then the
+   remaining rows one at a time. */
 template <int FMT, int R, int U>
 __device__ __forceinline__ void rows16(const DevMat& d, int64_t r0, int64_t r1, int32_t token,
                                        int lane) {
-    const u32x4* __restrict__ W = static_cast<const u32x4*>(d.w);
-    const u32x4* __restrict__ x =
-        reinterpret_cast<const u32x4*>(static_cast<const char*>(d.x) + token * d.x_stride);
-    float* __restrict__ y = reinterpret_cast<float*>(reinterpret_cast<char*>(d.y) + token * d.y_stride);
-    const int64_t nc = d.nc;
-    constexpr int STEP = WAVE * U;
-    for (int64_t i = r0; i < r1; i += R) {
-        float acc[R];
-#pragma unroll
-        for (int r = 0; r < R; ++r) acc[r] = 0.f;
-        for (int64_t c0 = 0; c0 < nc; c0 += STEP) {
-            u32x4 xv[U], wv[R][U];
-            if (c0 + STEP <= nc) {
-#pragma unroll
-                for (int u = 0; u < U; ++u) xv[u] = load_reused(x + c0 + u * WAVE + lane);
-#pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    if (i + r < r1) {
-                        const u32x4* wr = W + (i + r) * nc + c0 + lane;
-#pragma unroll
-                        for (int u = 0; u < U; ++u) wv[r][u] = load_once(wr + u * WAVE);
-                    } else {
-#pragma unroll
-                        for (int u = 0; u < U; ++u) wv[r][u] = zero4();
-                    }
-                }
-            } else {
-#pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const int64_t c = c0 + u * WAVE + lane;
-                    xv[u] = c < nc ? load_reused(x + c) : zero4();
-                }
-#pragma unroll
-                for (int r = 0; r < R; ++r) {
-#pragma unroll
-                    for (int u = 0; u < U; ++u) {
-                        const int64_t c = c0 + u * WAVE + lane;
-                        wv[r][u] = (i + r < r1 && c < nc) ? load_once(W + (i + r) * nc + c) : zero4();
-                    }
-                }
-            }
-#pragma unroll
-            for (int r = 0; r < R; ++r)
-#pragma unroll
-                for (int u = 0; u < U; ++u) acc[r] = dot8<FMT>(wv[r][u], xv[u], acc[r]);
-        }
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const float s = wave_sum(acc[r]);
-            if (lane == 0 && i + r < r1) y[i + r] = s;
-        }
-    }
+    const char* W = static_cast<const char*>(d.w);
+    g_u32x4* x = as_global<g_u32x4*>(static_cast<const char*>(d.x) + token * d.x_stride);
+    g_f32* y = as_global<g_f32*>(reinterpret_cast<char*>(d.y) + token * d.y_stride);
+    int64_t i = r0;
+    for (; i + R <= r1; i += R) group16<FMT, R, U>(W, x, y, d.nc, i, lane);
+    for (; i < r1; ++i) group16<FMT, 1, U>(W, x, y, d.nc, i, lane);
 }
 
 /* ---- q4 rows -----------------------------------------------------------------------------------
@@ -167,24 +187,26 @@ __device__ __forceinline__ void rows16(const DevMat& d, int64_t r0, int64_t r1, 
 
    In-register decode: with v = q + 8 (the code XOR 8), masking a code word with 0x000F000F gives
    two fp16 subnormals v * 2^-24 (elements k and k + 4), and 0x00F000F0 gives 16 v * 2^-24; the
-   same masks after a shift by 8 give the other two pairs, so one AND per pair decodes the word and
-   the values are exact.  Packed dot products with activation pairs then sum, per block,
-   Se = 2^-24 (sum_even q x + 8 Xe) and So = 2^-20 (sum_odd q x + 8 Xo), with Xe and Xo the
-   block's activation sums over even and odd k; the offset terms are computed once per block from
-   the activations alone and subtracted, and the block scale times 2^24 (exact) multiplies the
-   result.  The offset is small (8 Xe, not the value magnitude 1024 + v of a normal fp16), so the
-   fp32 sums keep nearly full precision, and a unit activation vector gives y = q * s exactly.
-*/
+   same masks after a shift by 8 give the other two pairs.  XOR and AND fuse into one three-input
+   bit operation, so a code word of 8 weights costs four bit operations, one shift and four packed
+   dot products, and the decoded values are exact.  Per block the dot products sum to
+   Se = 2^-24 (sum_even q x + 8 Xe) and So = 2^-20 (sum_odd q x + 8 Xo), Xe and Xo being the block's
+   activation sums over even and odd k; Se + So / 16 - 2^-24 (8 Xe + 8 Xo) is sum q x in units of
+   2^-24, where the offset term depends on the activations only and is formed once per block and
+   shared by the R rows.  The row total is scaled by 2^24 at the end (exact).  The offset is small
+   (8 times an activation sum), so the fp32 sums keep nearly full precision, and a unit activation
+   vector gives y = q * s exactly. */
+constexpr uint32_t Q4_SIGN = 0x88888888u;
 constexpr uint32_t Q4_LO = 0x000F000Fu, Q4_HI = 0x00F000F0u;
 constexpr uint32_t F16_OFS_EVEN = 0x00080008u;   /* 8 * 2^-24 in both halves (fp16 subnormal)   */
 constexpr uint32_t F16_OFS_ODD = 0x00800080u;    /* 16 * 8 * 2^-24                              */
 
 /* Activation pairs of one block, in the order the decode produces weights: for code dword d,
    p[4d] = (x[8d], x[8d+4]), p[4d+1] = (x[8d+1], x[8d+5]), p[4d+2] = (x[8d+2], x[8d+6]),
-   p[4d+3] = (x[8d+3], x[8d+7]); plus the even/odd offset terms. */
+   p[4d+3] = (x[8d+3], x[8d+7]); plus the block's offset term. */
 struct Q4X {
     uint32_t p[16];
-    float ce, co;
+    float off;
 };
 
 __device__ __forceinline__ void q4_prep(const u32x4 (&xv)[4], Q4X& q) {
@@ -204,80 +226,211 @@ __device__ __forceinline__ void q4_prep(const u32x4 (&xv)[4], Q4X& q) {
         ce = dot2<FMT_F16>(F16_OFS_EVEN, q.p[4 * d + 2], ce);
         co = dot2<FMT_F16>(F16_OFS_ODD, q.p[4 * d + 3], co);
     }
-    q.ce = ce;
-    q.co = co;
+    q.off = __builtin_fmaf(co, 0.0625f, ce);
 }
 
+/* sum_k q x over one block, in units of 2^-24. */
 __device__ __forceinline__ float q4_block_dot(u32x4 w, const Q4X& q) {
     float se = 0.f, so = 0.f;
     const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
-        const uint32_t t = wd[d] ^ 0x88888888u;
-        const uint32_t t8 = t >> 8;
-        se = dot2<FMT_F16>(t & Q4_LO, q.p[4 * d + 0], se);
-        so = dot2<FMT_F16>(t & Q4_HI, q.p[4 * d + 1], so);
-        se = dot2<FMT_F16>(t8 & Q4_LO, q.p[4 * d + 2], se);
-        so = dot2<FMT_F16>(t8 & Q4_HI, q.p[4 * d + 3], so);
+        const uint32_t w0 = wd[d], w8 = wd[d] >> 8;
+        se = dot2<FMT_F16>((w0 ^ Q4_SIGN) & Q4_LO, q.p[4 * d + 0], se);
+        so = dot2<FMT_F16>((w0 ^ Q4_SIGN) & Q4_HI, q.p[4 * d + 1], so);
+        se = dot2<FMT_F16>((w8 ^ Q4_SIGN) & Q4_LO, q.p[4 * d + 2], se);
+        so = dot2<FMT_F16>((w8 ^ Q4_SIGN) & Q4_HI, q.p[4 * d + 3], so);
     }
-    return (se - q.ce) + (so - q.co) * 0.0625f;   /* sum_k q x, in units of 2^-24 */
+    return __builtin_fmaf(so, 0.0625f, se) - q.off;
 }
 
-/* fp16 block scale times 2^24 (exact), undoing the 2^-24 unit of the decoded values. */
-__device__ __forceinline__ float q4_scale(uint16_t b) {
-    return (float)__builtin_bit_cast(_Float16, b) * 16777216.0f;
+__device__ __forceinline__ float f16_bits_to_f32(uint16_t b) {
+    return (float)__builtin_bit_cast(_Float16, b);
+}
+
+/* Registers of one step of R rows: U blocks per lane, their scales and the activations. */
+template <int R, int U>
+struct Q4Step {
+    u32x4 w[R][U];
+    uint16_t s[R][U];
+    u32x4 x[U][4];
+};
+
+/* Loads of the step at block b0 for rows wr[r] / sr[r] (all U * 64 blocks inside the row). */
+template <int R, int U>
+__device__ __forceinline__ void q4_load(Q4Step<R, U>& st, g_u32x4* const (&wr)[R], g_u16* const (&sr)[R],
+                                        g_u32x4* x, int64_t b0, int lane) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) st.x[u][j] = load_reused(x + 4 * (b0 + u * WAVE + lane) + j);
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            st.w[r][u] = load_once(wr[r] + b0 + u * WAVE + lane);
+            st.s[r][u] = sr[r][b0 + u * WAVE + lane];
+        }
+}
+
+/* Same, for a ragged last step: lanes past the row end load nothing and contribute zero. */
+template <int R, int U>
+__device__ __forceinline__ void q4_load_masked(Q4Step<R, U>& st, g_u32x4* const (&wr)[R],
+                                               g_u16* const (&sr)[R], g_u32x4* x, int64_t b0,
+                                               int64_t nb, int lane) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t b = b0 + u * WAVE + lane;
+        const bool ok = b < nb;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) st.x[u][j] = ok ? load_reused(x + 4 * b + j) : zero4();
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            st.w[r][u] = ok ? load_once(wr[r] + b) : zero4();
+            st.s[r][u] = ok ? sr[r][b] : (uint16_t)0;
+        }
+    }
 }
 
 template <int R, int U>
+__device__ __forceinline__ void q4_compute(const Q4Step<R, U>& st, float (&acc)[R]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        Q4X q;
+        q4_prep(st.x[u], q);
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+            acc[r] = __builtin_fmaf(f16_bits_to_f32(st.s[r][u]), q4_block_dot(st.w[r][u], q), acc[r]);
+    }
+}
+
+template <int R>
+__device__ __forceinline__ void q4_store(g_f32* y, int64_t i, float (&acc)[R], int lane) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const float s = wave_sum(acc[r]) * 16777216.0f;   /* undo the 2^-24 unit (exact) */
+        if (lane == 0) y[i + r] = s;
+        acc[r] = 0.f;
+    }
+}
+
+/* Rows [i, i + R), any block count: one step at a time. */
+template <int R, int U>
+__device__ __forceinline__ void q4_group(g_u32x4* Wq, g_u16* S, g_u32x4* x, g_f32* y, int64_t nb,
+                                         int64_t i, int lane) {
+    constexpr int STEP = WAVE * U;
+    float acc[R];
+    g_u32x4* wr[R];
+    g_u16* sr[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        acc[r] = 0.f;
+        wr[r] = Wq + (i + r) * nb;
+        sr[r] = S + (i + r) * nb;
+    }
+    for (int64_t b0 = 0; b0 < nb; b0 += STEP) {
+        Q4Step<R, U> st;
+        if (b0 + STEP <= nb) q4_load<R, U>(st, wr, sr, x, b0, lane);
+        else q4_load_masked<R, U>(st, wr, sr, x, b0, nb, lane);
+        q4_compute<R, U>(st, acc);
+    }
+    q4_store<R>(y, i, acc, lane);
+}
+
+/* Rows [r0, r1) of a q4 matrix.  When rows hold whole steps (nb a multiple of 64 U) the groups of
+   R rows run as one software pipeline: the loads of the next step (of this row group or the
+   next one) are issued before the current step is decoded, two register sets taking turns, so
+   every wave keeps memory requests in flight while it computes.  Remaining rows go one at a
+   time. */
+template <int R, int U>
 __device__ __forceinline__ void rows_q4(const DevMat& d, int64_t r0, int64_t r1, int32_t token,
                                         int lane) {
-    const u32x4* __restrict__ Wq = static_cast<const u32x4*>(d.w);
-    const uint16_t* __restrict__ S = static_cast<const uint16_t*>(d.s);
-    const u32x4* __restrict__ x =
-        reinterpret_cast<const u32x4*>(static_cast<const char*>(d.x) + token * d.x_stride);
-    float* __restrict__ y = reinterpret_cast<float*>(reinterpret_cast<char*>(d.y) + token * d.y_stride);
+    g_u32x4* Wq = as_global<g_u32x4*>(d.w);
+    g_u16* S = as_global<g_u16*>(d.s);
+    g_u32x4* x = as_global<g_u32x4*>(static_cast<const char*>(d.x) + token * d.x_stride);
+    g_f32* y = as_global<g_f32*>(reinterpret_cast<char*>(d.y) + token * d.y_stride);
     const int64_t nb = d.nc;
     constexpr int STEP = WAVE * U;
-    for (int64_t i = r0; i < r1; i += R) {
+    const int64_t ngroups = (r1 - r0) / R;
+    int64_t i_end = r0 + ngroups * R;
+    if (ngroups > 0 && nb % STEP == 0 && nb > 0) {
+        const int64_t steps = nb / STEP;                 /* steps per row group */
+        g_u32x4* wr[R];
+        g_u16* sr[R];
+        auto point = [&](int64_t g) {                    /* row pointers of group g */
+            const int64_t i = r0 + g * R;
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                wr[r] = Wq + (i + r) * nb;
+                sr[r] = S + (i + r) * nb;
+            }
+        };
         float acc[R];
 #pragma unroll
         for (int r = 0; r < R; ++r) acc[r] = 0.f;
-        for (int64_t b0 = 0; b0 < nb; b0 += STEP) {
-            u32x4 xv[U][4], wv[R][U];
-            uint16_t sv[R][U];
-            bool ok[U];
-#pragma unroll
-            for (int u = 0; u < U; ++u) ok[u] = b0 + u * WAVE + lane < nb;
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int64_t b = b0 + u * WAVE + lane;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) xv[u][j] = ok[u] ? load_reused(x + 4 * b + j) : zero4();
-            }
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-#pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    const int64_t b = b0 + u * WAVE + lane;
-                    const bool live = i + r < r1 && ok[u];
-                    wv[r][u] = live ? load_once(Wq + (i + r) * nb + b) : zero4();
-                    sv[r][u] = live ? S[(i + r) * nb + b] : (uint16_t)0;
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                Q4X q;
-                q4_prep(xv[u], q);
-#pragma unroll
-                for (int r = 0; r < R; ++r)
-                    acc[r] = __builtin_fmaf(q4_scale(sv[r][u]), q4_block_dot(wv[r][u], q), acc[r]);
-            }
+        Q4Step<R, U> A, B;
+        int64_t g = 0, k = 0;                            /* (group, step) of the unit in A */
+        point(0);
+        q4_load<R, U>(A, wr, sr, x, 0, lane);
+        for (;;) {
+            int64_t g1 = g, k1 = k + 1;
+            if (k1 == steps) { k1 = 0; ++g1; }
+            bool more = g1 < ngroups;
+            if (more) { point(g1); q4_load<R, U>(B, wr, sr, x, k1 * STEP, lane); }
+            __builtin_amdgcn_sched_barrier(0);           /* keep those loads ahead of the decode */
+            q4_compute<R, U>(A, acc);
+            if (k + 1 == steps) q4_store<R>(y, r0 + g * R, acc, lane);
+            if (!more) break;
+            g = g1; k = k1;                              /* the unit in B */
+            g1 = g; k1 = k + 1;
+            if (k1 == steps) { k1 = 0; ++g1; }
+            more = g1 < ngroups;
+            if (more) { point(g1); q4_load<R, U>(A, wr, sr, x, k1 * STEP, lane); }
+            __builtin_amdgcn_sched_barrier(0);
+            q4_compute<R, U>(B, acc);
+            if (k + 1 == steps) q4_store<R>(y, r0 + g * R, acc, lane);
+            if (!more) break;
+            g = g1; k = k1;                              /* the unit in A */
         }
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const float s = wave_sum(acc[r]);
-            if (lane == 0 && i + r < r1) y[i + r] = s;
+    } else {
+        i_end = r0;
+    }
+    for (int64_t i = i_end; i < r1; ++i) q4_group<1, U>(Wq, S, x, y, nb, i, lane);
+}
+
+/* ---- ranges of the weight stream ---------------------------------------------------------------
+
+   The rows of a table of matrices, in table order, form one weight stream; a row belongs to the byte
+   range that holds its first byte.  `hint` carries the matrix index of the previous range of the
+   same wave, so increasing ranges resume where the last one ended. */
+__device__ __forceinline__ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+template <int FMT, int R16, int U16, int RQ, int UQ>
+__device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, int nmat, int64_t lo,
+                                             int64_t hi, int32_t token, int lane, int& hint) {
+    int a = hint;
+    if (tab[a].cost0 > lo) a = 0;
+    if (a + 1 < nmat && tab[a + 1].cost0 <= lo) {   /* last matrix whose stream starts <= lo */
+        int b = nmat - 1;
+        while (a < b) {
+            const int mid = (a + b + 1) >> 1;
+            if (tab[mid].cost0 <= lo) a = mid; else b = mid - 1;
         }
+    }
+    for (int m = a; m < nmat; ++m) {
+        const DevMat d = tab[m];
+        if (d.cost0 >= hi) break;
+        hint = m;
+        const int64_t r0 = lo > d.cost0 ? ceil_div(lo - d.cost0, d.row_bytes) : 0;
+        const int64_t r1 = d.M < ceil_div(hi - d.cost0, d.row_bytes) ? d.M : ceil_div(hi - d.cost0, d.row_bytes);
+        if (r0 >= r1) continue;
+        const int fmt = FMT ? FMT : d.fmt;
+        if ((FMT == 0 || FMT == FMT_F16) && fmt == FMT_F16)
+            rows16<FMT_F16, R16, U16>(d, r0, r1, token, lane);
+        else if ((FMT == 0 || FMT == FMT_BF16) && fmt == FMT_BF16)
+            rows16<FMT_BF16, R16, U16>(d, r0, r1, token, lane);
+        else if ((FMT == 0 || FMT == FMT_Q4) && fmt == FMT_Q4)
+            rows_q4<RQ, UQ>(d, r0, r1, token, lane);
     }
 }
 

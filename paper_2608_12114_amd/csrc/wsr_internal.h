@@ -35,9 +35,13 @@ hipError_t launch_probe(const float* buf, int64_t n, double* sum_dev, void* ws, 
 int64_t probe_grid(int64_t n);
 
 hipError_t launch_gemv(const DevMat& m, hipStream_t s);
-hipError_t launch_put_table(DevMat* dst, const DevMat* src, int n, hipStream_t s);
+/* Writes the table and clears the two tile counters at ctr (ctr may be null). */
+hipError_t launch_put_table(DevMat* dst, const DevMat* src, int n, unsigned* ctr, hipStream_t s);
 hipError_t launch_sweep(const DevMat* tab, int nmat, int64_t total_bytes, int fmt_all,
-                        int32_t token, hipStream_t s);
+                        int32_t token, unsigned* ctr, hipStream_t s);
+
+/* Sweep workspace: tile counters in the first SWEEP_CTR_BYTES, then the table. */
+constexpr size_t SWEEP_CTR_BYTES = 256;
 
 }  // namespace wsr
 

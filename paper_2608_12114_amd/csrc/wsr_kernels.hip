@@ -1,12 +1,17 @@
 /*
  * wsr_kernels.hip - HIP kernels of the weight-streaming read path for gfx950 and their launchers.
  *
- *  k_probe     pure-read reference: fp32 buffer -> fp64 sum (Sec. 3.1, 3.3 of the paper)
+ *  k_probe_part / k_probe_final   pure-read reference: fp32 buffer -> fp64 sum (paper Sec. 3.1, 3.3)
  *  k_gemv16    single-token GEMV, fp16 / bf16 weights and activations, fp32 accumulate (Sec. 3.1)
  *  k_gemv_q4   single-token GEMV over 4-bit block-quantised weights, decoded in registers
- *  k_sweep     one decode token: every matrix of the model in one persistent launch (Sec. 6.2)
- *  k_put_table writes the sweep's matrix table into the caller's workspace from kernel arguments,
- *              so a sweep needs no host-side copy or synchronisation (C3, Table 1)
+ *  k_sweep     one decode token: every matrix of a table in one persistent launch (Sec. 6.2)
+ *  k_put_table writes the sweep's matrix table into the caller's workspace from kernel arguments
+ *              and clears the sweep's tile counters, so a sweep needs no host copy or host
+ *              synchronisation (C3, Table 1)
+ *
+ * Streaming layout.  HBM3E serves long sequential runs best: each probe block walks its own
+ * contiguous region, and the sweep hands out 1 MiB tiles of the weight stream in order, so the
+ * waves in flight all work on one moving front of memory.
  */
 #include <hip/hip_runtime.h>
 
@@ -16,16 +21,18 @@
 
 namespace wsr {
 
+constexpr int BLOCK = 256;
+constexpr int WAVES_PER_BLOCK = BLOCK / WAVE;
+
 /* ======================================= probe ================================================ */
 
-constexpr int PROBE_BLOCK = 256;
-constexpr int PROBE_UNROLL = 8;
-constexpr int64_t PROBE_MAX_GRID = 2048;   /* 8 blocks per CU on a 256-CU part */
-constexpr int64_t PROBE_PART_OFFSET = 64;  /* ws: [ticket | pad to 64 B][fp64 partial per block] */
+constexpr int PROBE_UNROLL = 4;            /* 16-byte loads in flight per thread               */
+constexpr int PROBE_ACC = 4;               /* independent fp64 accumulators per thread          */
+constexpr int64_t PROBE_MAX_GRID = 512;    /* two blocks per CU: few, long sequential streams   */
 
 int64_t probe_grid(int64_t n) {
     const int64_t n4 = n / 4;
-    const int64_t per_block = (int64_t)PROBE_BLOCK * PROBE_UNROLL;
+    const int64_t per_block = (int64_t)BLOCK * PROBE_UNROLL * 4;
     const int64_t g = (n4 + per_block - 1) / per_block;
     return std::max<int64_t>(1, std::min(g, PROBE_MAX_GRID));
 }
@@ -40,81 +47,79 @@ __device__ __forceinline__ double sum4(u32x4 v, double acc) {
     return acc;
 }
 
-/* Sum of a block's values in thread order of waves: valid in thread 0. */
+/* Sum over a block's threads, in a fixed order: valid in thread 0. */
 __device__ __forceinline__ double block_sum(double v, double* red) {
     v = wave_sum(v);
-    const int w = threadIdx.x / WAVE;
-    if ((threadIdx.x & (WAVE - 1)) == 0) red[w] = v;
+    if ((threadIdx.x & (WAVE - 1)) == 0) red[threadIdx.x / WAVE] = v;
     __syncthreads();
     double s = 0.0;
     if (threadIdx.x == 0)
-        for (int i = 0; i < PROBE_BLOCK / WAVE; ++i) s += red[i];
+        for (int i = 0; i < WAVES_PER_BLOCK; ++i) s += red[i];
     return s;
 }
 
-/* Grid-stride over 16-byte groups: thread t of block b reads groups b*256 + t + j*stride.  Each
-   block publishes one fp64 partial; the last block to take a ticket adds the partials in index order
-   (plus the n % 4 tail) and resets the ticket for the next call. */
-__global__ __launch_bounds__(PROBE_BLOCK) void k_probe(const u32x4* __restrict__ buf, int64_t n4,
-                                                       int ntail, double* __restrict__ part,
-                                                       unsigned* __restrict__ ticket,
-                                                       double* __restrict__ out) {
-    __shared__ double red[PROBE_BLOCK / WAVE];
-    __shared__ int last;
-    const int64_t stride = (int64_t)gridDim.x * PROBE_BLOCK;
-    int64_t i = (int64_t)blockIdx.x * PROBE_BLOCK + threadIdx.x;
-    double acc = 0.0;
-    for (; i + (PROBE_UNROLL - 1) * stride < n4; i += PROBE_UNROLL * stride) {
+/* Block b sums 16-byte groups [b * chunk, (b + 1) * chunk): per step its 256 threads read 16 KiB of
+   consecutive memory, thread t taking groups t, t + 256, t + 512, t + 768 into accumulators 0..3. */
+__global__ __launch_bounds__(BLOCK) void k_probe_part(const u32x4* __restrict__ buf, int64_t n4,
+                                                      double* __restrict__ part) {
+    __shared__ double red[WAVES_PER_BLOCK];
+    g_u32x4* b = as_global<g_u32x4*>(buf);
+    const int64_t chunk = (n4 + gridDim.x - 1) / gridDim.x;
+    const int64_t beg = (int64_t)blockIdx.x * chunk;
+    const int64_t end = std::min<int64_t>(n4, beg + chunk);
+    double acc[PROBE_ACC];
+#pragma unroll
+    for (int a = 0; a < PROBE_ACC; ++a) acc[a] = 0.0;
+    int64_t i = beg + threadIdx.x;
+    for (; i + (PROBE_UNROLL - 1) * BLOCK < end; i += PROBE_UNROLL * BLOCK) {
         u32x4 v[PROBE_UNROLL];
 #pragma unroll
-        for (int j = 0; j < PROBE_UNROLL; ++j) v[j] = load_once(buf + i + j * stride);
+        for (int j = 0; j < PROBE_UNROLL; ++j) v[j] = load_once(b + i + j * BLOCK);
 #pragma unroll
-        for (int j = 0; j < PROBE_UNROLL; ++j) acc = sum4(v[j], acc);
+        for (int j = 0; j < PROBE_UNROLL; ++j) acc[j % PROBE_ACC] = sum4(v[j], acc[j % PROBE_ACC]);
     }
-    for (; i < n4; i += stride) acc = sum4(load_once(buf + i), acc);
+    for (; i < end; i += BLOCK) acc[0] = sum4(load_once(b + i), acc[0]);
+    double t = 0.0;
+#pragma unroll
+    for (int a = 0; a < PROBE_ACC; ++a) t += acc[a];
+    t = block_sum(t, red);
+    if (threadIdx.x == 0) part[blockIdx.x] = t;
+}
 
-    const double b = block_sum(acc, red);
-    if (threadIdx.x == 0) {
-        __hip_atomic_store(part + blockIdx.x, b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __threadfence();
-        const unsigned t = __hip_atomic_fetch_add(ticket, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-        last = (t == gridDim.x - 1);
-    }
-    __syncthreads();
-    if (!last) return;
-    __threadfence();
+/* One block: the partials in index order, then the n % 4 trailing elements. */
+__global__ __launch_bounds__(BLOCK) void k_probe_final(const double* __restrict__ part, int G,
+                                                       const float* __restrict__ tail, int ntail,
+                                                       double* __restrict__ out) {
+    __shared__ double red[WAVES_PER_BLOCK];
     double a = 0.0;
-    for (int64_t j = threadIdx.x; j < (int64_t)gridDim.x; j += PROBE_BLOCK)
-        a += __hip_atomic_load(part + j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __syncthreads();  /* red[] is reused */
+    for (int j = threadIdx.x; j < G; j += BLOCK) a += part[j];
     double s = block_sum(a, red);
     if (threadIdx.x == 0) {
-        const float* tail = reinterpret_cast<const float*>(buf + n4);
         for (int j = 0; j < ntail; ++j) s += (double)tail[j];
         *out = s;
-        __hip_atomic_store(ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 
 hipError_t launch_probe(const float* buf, int64_t n, double* sum_dev, void* ws, hipStream_t s) {
     const int64_t g = probe_grid(n);
-    unsigned* ticket = static_cast<unsigned*>(ws);
-    double* part = reinterpret_cast<double*>(static_cast<char*>(ws) + PROBE_PART_OFFSET);
-    hipLaunchKernelGGL(k_probe, dim3((unsigned)g), dim3(PROBE_BLOCK), 0, s,
-                       reinterpret_cast<const u32x4*>(buf), n / 4, (int)(n % 4), part, ticket, sum_dev);
+    const int64_t n4 = n / 4;
+    double* part = static_cast<double*>(ws);
+    hipLaunchKernelGGL(k_probe_part, dim3((unsigned)g), dim3(BLOCK), 0, s,
+                       reinterpret_cast<const u32x4*>(buf), n4, part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_probe_final, dim3(1), dim3(BLOCK), 0, s, part, (int)g, buf + 4 * n4,
+                       (int)(n % 4), sum_dev);
     return hipGetLastError();
 }
 
 /* ======================================= GEMVs ================================================ */
 
-constexpr int BLOCK = 256;
-constexpr int WAVES_PER_BLOCK = BLOCK / WAVE;
-
 /* One wave per R consecutive rows. */
 template <int FMT, int R, int U>
 __global__ __launch_bounds__(BLOCK) void k_gemv16(DevMat d) {
     const int lane = threadIdx.x & (WAVE - 1);
-    const int64_t wave = (int64_t)blockIdx.x * WAVES_PER_BLOCK + threadIdx.x / WAVE;
+    const int64_t wave = (int64_t)blockIdx.x * WAVES_PER_BLOCK + wave_in_block();
     const int64_t r0 = wave * R;
     if (r0 >= d.M) return;
     rows16<FMT, R, U>(d, r0, std::min<int64_t>(r0 + R, d.M), 0, lane);
@@ -123,7 +128,7 @@ __global__ __launch_bounds__(BLOCK) void k_gemv16(DevMat d) {
 template <int R, int U>
 __global__ __launch_bounds__(BLOCK) void k_gemv_q4(DevMat d) {
     const int lane = threadIdx.x & (WAVE - 1);
-    const int64_t wave = (int64_t)blockIdx.x * WAVES_PER_BLOCK + threadIdx.x / WAVE;
+    const int64_t wave = (int64_t)blockIdx.x * WAVES_PER_BLOCK + wave_in_block();
     const int64_t r0 = wave * R;
     if (r0 >= d.M) return;
     rows_q4<R, U>(d, r0, std::min<int64_t>(r0 + R, d.M), 0, lane);
@@ -141,13 +146,12 @@ hipError_t launch_gemv(const DevMat& m, hipStream_t s) {
     if (m.M == 0) return hipSuccess;
     switch (m.fmt) {
         case FMT_F16:
-            return m.M >= 8192 ? launch_rows(k_gemv16<FMT_F16, 2, 8>, m, 2, s)
-                               : launch_rows(k_gemv16<FMT_F16, 1, 8>, m, 1, s);
+            return launch_rows(k_gemv16<FMT_F16, 1, 4>, m, 1, s);
         case FMT_BF16:
-            return m.M >= 8192 ? launch_rows(k_gemv16<FMT_BF16, 2, 8>, m, 2, s)
-                               : launch_rows(k_gemv16<FMT_BF16, 1, 8>, m, 1, s);
+            return launch_rows(k_gemv16<FMT_BF16, 1, 4>, m, 1, s);
         case FMT_Q4:
-            return launch_rows(k_gemv_q4<4, 1>, m, 4, s);
+            return m.nc >= 256 ? launch_rows(k_gemv_q4<2, 2>, m, 2, s)
+                               : launch_rows(k_gemv_q4<4, 1>, m, 4, s);
         default:
             return hipErrorInvalidValue;
     }
@@ -162,54 +166,67 @@ struct TableChunk {
     DevMat m[TABLE_CHUNK];
 };
 
-__global__ __launch_bounds__(WAVE) void k_put_table(DevMat* __restrict__ dst, TableChunk c) {
+__global__ __launch_bounds__(WAVE) void k_put_table(DevMat* __restrict__ dst, TableChunk c,
+                                                    unsigned* __restrict__ ctr) {
     const int i = threadIdx.x;
     if (i < c.n) dst[i] = c.m[i];
+    if (ctr && i < 2) ctr[i] = 0u;
 }
 
-hipError_t launch_put_table(DevMat* dst, const DevMat* src, int n, hipStream_t s) {
+hipError_t launch_put_table(DevMat* dst, const DevMat* src, int n, unsigned* ctr, hipStream_t s) {
     for (int first = 0; first < n; first += TABLE_CHUNK) {
         TableChunk c{};
         c.n = std::min(TABLE_CHUNK, n - first);
         for (int i = 0; i < c.n; ++i) c.m[i] = src[first + i];
-        hipLaunchKernelGGL(k_put_table, dim3(1), dim3(WAVE), 0, s, dst + first, c);
+        hipLaunchKernelGGL(k_put_table, dim3(1), dim3(WAVE), 0, s, dst + first, c, first == 0 ? ctr : nullptr);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
 }
 
-__device__ __forceinline__ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+/* Schedules over the weight stream of one launch (`total` bytes):
+   TILES  waves take tiles of `tile` bytes in order from a counter (ctr[0]); a wave that finds none
+          left checks out on ctr[1], and the last one resets both for the next launch.
+   SPANS  wave w of nw owns [w * total / nw, (w + 1) * total / nw) (no counters).
+   Every row has exactly one owner either way, and its result does not depend on the owner. */
+enum : int { SCHED_TILES = 0, SCHED_SPANS = 1 };
 
-/* Rows of all matrices, in table order, form one weight stream of `total` bytes.  Wave w of nw owns
-   the rows whose first byte lies in [w * total / nw, (w + 1) * total / nw), so every wave streams
-   the same number of bytes and every row has exactly one owner. */
-template <int FMTALL>
-__global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab, int nmat,
-                                                 int64_t total, int32_t token) {
+/* Tile size: about four tiles per wave, a power of two between 64 KiB and 1 MiB. */
+int64_t sweep_tile(int64_t total, int64_t waves) {
+    int64_t t = 64 << 10;
+    while (t < (1 << 20) && t * waves * 4 < total) t <<= 1;
+    return t;
+}
+
+template <int FMT, int SCHED, int R16, int U16, int RQ, int UQ>
+__global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab, int nmat, int64_t total,
+                                                 int64_t tile, int32_t token, unsigned* __restrict__ ctr) {
     const int lane = threadIdx.x & (WAVE - 1);
-    const int64_t nw = (int64_t)gridDim.x * WAVES_PER_BLOCK;
-    const int64_t w = (int64_t)blockIdx.x * WAVES_PER_BLOCK + threadIdx.x / WAVE;
-    const int64_t lo = total * w / nw, hi = total * (w + 1) / nw;
-    if (lo >= hi) return;
-    int a = 0, b = nmat - 1;  /* last matrix whose stream starts at or before lo */
-    while (a < b) {
-        const int mid = (a + b + 1) >> 1;
-        if (tab[mid].cost0 <= lo) a = mid; else b = mid - 1;
-    }
-    for (int m = a; m < nmat; ++m) {
-        const DevMat d = tab[m];
-        if (d.cost0 >= hi) break;
-        const int64_t r0 = lo > d.cost0 ? ceil_div(lo - d.cost0, d.row_bytes) : 0;
-        const int64_t r1 = std::min<int64_t>(d.M, ceil_div(hi - d.cost0, d.row_bytes));
-        if (r0 >= r1) continue;
-        const int fmt = FMTALL ? FMTALL : d.fmt;
-        if ((FMTALL == 0 || FMTALL == FMT_F16) && fmt == FMT_F16)
-            rows16<FMT_F16, 2, 4>(d, r0, r1, token, lane);
-        else if ((FMTALL == 0 || FMTALL == FMT_BF16) && fmt == FMT_BF16)
-            rows16<FMT_BF16, 2, 4>(d, r0, r1, token, lane);
-        else if ((FMTALL == 0 || FMTALL == FMT_Q4) && fmt == FMT_Q4)
-            rows_q4<4, 1>(d, r0, r1, token, lane);
+    const unsigned nw = gridDim.x * WAVES_PER_BLOCK;
+    int hint = 0;
+    if constexpr (SCHED == SCHED_SPANS) {
+        const int64_t w = (int64_t)blockIdx.x * WAVES_PER_BLOCK + wave_in_block();
+        const int64_t lo = total * w / nw, hi = total * (w + 1) / nw;
+        if (lo < hi) stream_range<FMT, R16, U16, RQ, UQ>(tab, nmat, lo, hi, token, lane, hint);
+    } else {
+        const int64_t ntiles = ceil_div(total, tile);
+        for (;;) {
+            unsigned t = 0;
+            if (lane == 0) t = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            t = __builtin_amdgcn_readfirstlane(t);
+            if ((int64_t)t >= ntiles) break;
+            const int64_t lo = (int64_t)t * tile;
+            stream_range<FMT, R16, U16, RQ, UQ>(tab, nmat, lo, std::min<int64_t>(total, lo + tile), token,
+                                                lane, hint);
+        }
+        if (lane == 0) {
+            const unsigned e = __hip_atomic_fetch_add(ctr + 1, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+            if (e == nw - 1) {
+                __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(ctr + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
     }
 }
 
@@ -226,22 +243,30 @@ static int cu_count() {
     return cache[dev];
 }
 
+/* 16-bit weights: tiles, 4 rows x 4 KiB steps per wave, two blocks per CU (few, long streams);
+   q4: spans, 8 rows x 1 block per lane per step (eight rows share each block's activation
+   decode), software-pipelined. */
+constexpr int SWEEP_BLOCKS_PER_CU_16 = 2;
+constexpr int SWEEP_BLOCKS_PER_CU_Q4 = 4;
+
 hipError_t launch_sweep(const DevMat* tab, int nmat, int64_t total, int fmt_all, int32_t token,
-                        hipStream_t s) {
+                        unsigned* ctr, hipStream_t s) {
     if (nmat == 0 || total == 0) return hipSuccess;
-    const unsigned blocks = (unsigned)cu_count() * 4;
+    const int bpc = fmt_all == FMT_Q4 ? SWEEP_BLOCKS_PER_CU_Q4 : SWEEP_BLOCKS_PER_CU_16;
+    const dim3 grid((unsigned)(cu_count() * bpc)), block(BLOCK);
+    const int64_t tile = sweep_tile(total, (int64_t)grid.x * WAVES_PER_BLOCK);
     switch (fmt_all) {
         case FMT_F16:
-            hipLaunchKernelGGL(k_sweep<FMT_F16>, dim3(blocks), dim3(BLOCK), 0, s, tab, nmat, total, token);
+            hipLaunchKernelGGL((k_sweep<FMT_F16, SCHED_TILES, 4, 4, 8, 1>), grid, block, 0, s, tab, nmat, total, tile, token, ctr);
             break;
         case FMT_BF16:
-            hipLaunchKernelGGL(k_sweep<FMT_BF16>, dim3(blocks), dim3(BLOCK), 0, s, tab, nmat, total, token);
+            hipLaunchKernelGGL((k_sweep<FMT_BF16, SCHED_TILES, 4, 4, 8, 1>), grid, block, 0, s, tab, nmat, total, tile, token, ctr);
             break;
         case FMT_Q4:
-            hipLaunchKernelGGL(k_sweep<FMT_Q4>, dim3(blocks), dim3(BLOCK), 0, s, tab, nmat, total, token);
+            hipLaunchKernelGGL((k_sweep<FMT_Q4, SCHED_SPANS, 4, 4, 8, 1>), grid, block, 0, s, tab, nmat, total, tile, token, ctr);
             break;
         default:
-            hipLaunchKernelGGL(k_sweep<0>, dim3(blocks), dim3(BLOCK), 0, s, tab, nmat, total, token);
+            hipLaunchKernelGGL((k_sweep<0, SCHED_TILES, 4, 4, 8, 1>), grid, block, 0, s, tab, nmat, total, tile, token, ctr);
             break;
     }
     return hipGetLastError();

@@ -66,8 +66,8 @@ def test_gemv_argument_checks():
 def test_probe_argument_checks():
     f = "wsr_probe_read"
     need = wsr.wsr_probe_workspace_bytes(1 << 28)
-    assert need == 64 + 8 * 2048
-    assert wsr.wsr_probe_workspace_bytes(0) == 72 and wsr.wsr_probe_workspace_bytes(5) == 72
+    assert need == 8 * 512
+    assert wsr.wsr_probe_workspace_bytes(0) == 8 and wsr.wsr_probe_workspace_bytes(5) == 8
     assert _status(f, None, 8, A, A, need, None) == wsr.WSR_E_ARG
     assert _status(f, A, 8, None, A, need, None) == wsr.WSR_E_ARG
     assert _status(f, A + 4, 8, A, A, need, None) == wsr.WSR_E_ALIGN
@@ -79,7 +79,7 @@ def test_sweep_argument_checks():
     good = dict(fmt=2, M=8, K=64, w=A, x=A, y=A, x_tok_stride=128, y_tok_stride=32)
     mats = wsr.make_mats([good, dict(good, fmt=3, scales=A)])
     ws = wsr.wsr_sweep_workspace_bytes(mats)
-    assert ws == 256
+    assert ws == 256 + 256
     f = "wsr_decode_sweep"
     assert _status(f, mats, 2, 0, A, ws, None) == wsr.WSR_E_ARG             # n_tokens < 1
     assert _status(f, mats, 2, 1, A + 16, ws, None) == wsr.WSR_E_ALIGN      # ws 256-byte alignment
