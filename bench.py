@@ -36,6 +36,31 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+KERNEL_SOURCES = ("paper_2608_12114_amd/csrc/wsr_device.h", "paper_2608_12114_amd/csrc/wsr_kernels.hip",
+                  "paper_2608_12114_amd/csrc/wsr_internal.h")
+PROFILE_OF = {"llama70b_bf16": "k_sweep_bf16_llama70b", "llama8b_q4": "k_sweep_q4_llama8b"}
+
+
+def kernel_sources_sha256() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    return h.hexdigest()
+
+
+def profiled_traffic(workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary (FETCH_SIZE + WRITE_SIZE,
+    each scaled by the copy-kernel calibration), or None when the kernel sources changed since."""
+    path = os.path.join(ROOT, "profiles", PROFILE_OF[workload] + ".json")
+    if not os.path.exists(path):
+        return None, "no profile"
+    rec = json.load(open(path))
+    if rec.get("kernel_source_sha256") != kernel_sources_sha256():
+        return None, "kernel changed since the counters were taken"
+    return rec.get("traffic_bytes_per_launch"), os.path.relpath(path, ROOT)
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
@@ -354,6 +379,7 @@ def main():
 
     gbps = head["GBps"]
     dtype = {"llama70b_bf16": "bf16", "llama8b_q4": "q4+f16"}[args.workload]
+    traffic, traffic_src = profiled_traffic(args.workload)
     line = {
         "metric": "achieved GB/s (% of HBM peak) for decode-step GEMV sweep; tokens/s at batch 1",
         "value": round(gbps, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -366,7 +392,7 @@ def main():
                    "step": "one decode token: every projection matrix of every layer plus lm_head, one launch"},
         "tokens_per_s": round(head["tokens_per_s"], 3), "hbm_frac": round(head["hbm_frac"], 4),
         "roofline": {"bound": "hbm", "achieved": round(gbps, 2), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
-                     "frac": round(head["hbm_frac"], 4), "traffic": None,
+                     "frac": round(head["hbm_frac"], 4), "traffic": traffic, "traffic_source": traffic_src,
                      "kernel": f"k_sweep ({dtype})", "bytes_per_launch": head["bytes_per_token"]},
         "cpu_baseline": head.get("cpu_baseline"),
         "parity": head["parity"],

@@ -93,16 +93,60 @@ __device__ __forceinline__ double dpp_f64(double v) {
     return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
 }
 
-/* Butterfly sum over the 64 lanes.  Each step adds a value to its partner's, and a + b == b + a,
-   so all lanes end with the same bits and the association order is fixed. */
-__device__ __forceinline__ float wave_sum(float v) {
-    v += dpp_f32<DPP_XOR1>(v);
-    v += dpp_f32<DPP_XOR2>(v);
-    v += dpp_f32<DPP_HALF_MIRROR>(v);
-    v += dpp_f32<DPP_MIRROR>(v);
-    v += __shfl_xor(v, 16);
-    v += __shfl_xor(v, 32);
+/* Lane exchanges of the row reductions, in the order they are applied: lanes 32 apart, 16 apart,
+   mirrored inside each 16-lane row (i <-> 15 - i), then the two quad swaps and the mirror inside
+   each 8-lane half.  Each step pairs every lane with one partner, and together they join all 64. */
+template <int LEVEL>
+__device__ __forceinline__ float xchg(float v) {
+    if constexpr (LEVEL == 0) return __shfl_xor(v, 32);
+    else if constexpr (LEVEL == 1) return __shfl_xor(v, 16);
+    else if constexpr (LEVEL == 2) return dpp_f32<DPP_MIRROR>(v);
+    else if constexpr (LEVEL == 3) return dpp_f32<DPP_XOR1>(v);
+    else if constexpr (LEVEL == 4) return dpp_f32<DPP_XOR2>(v);
+    else return dpp_f32<DPP_HALF_MIRROR>(v);
+}
+
+/* One transposed step: lanes whose `bit` is set keep the upper half of the row list and send the
+   lower half to their partner, which keeps the lower half. */
+template <int LEVEL, int N>
+__device__ __forceinline__ void halve_rows(float (&a)[N], int n, bool upper) {
+    const int h = n / 2;
+#pragma unroll
+    for (int j = 0; j < N / 2; ++j) {
+        if (j < h) {
+            const float send = upper ? a[j] : a[j + h];
+            const float keep = upper ? a[j + h] : a[j];
+            a[j] = keep + xchg<LEVEL>(send);
+        }
+    }
+}
+
+/* Totals of R per-lane partial sums (R = 1, 2, 4 or 8 rows) over the 64 lanes.  The first log2(R)
+   exchanges split the rows between partner lanes instead of duplicating them, so a group of R rows
+   costs about as much as one row; afterwards lane l holds the total of row l / (64 / R).  Every
+   row is summed by the same tree of pairwise additions whatever R is (each step adds a lane's
+   partial to its partner's, and a + b == b + a), so results do not depend on how rows were
+   grouped. */
+template <int R>
+__device__ __forceinline__ float wave_sum_rows(float (&a)[R], int lane) {
+    static_assert(R == 1 || R == 2 || R == 4 || R == 8, "R must be 1, 2, 4 or 8");
+    if constexpr (R >= 2) halve_rows<0, R>(a, R, lane & 32);
+    if constexpr (R >= 4) halve_rows<1, R>(a, R / 2, lane & 16);
+    if constexpr (R >= 8) halve_rows<2, R>(a, R / 4, lane & 8);
+    float v = a[0];
+    if constexpr (R < 2) v += xchg<0>(v);
+    if constexpr (R < 4) v += xchg<1>(v);
+    if constexpr (R < 8) v += xchg<2>(v);
+    v += xchg<3>(v);
+    v += xchg<4>(v);
+    v += xchg<5>(v);
     return v;
+}
+
+/* Single-row form: every lane ends with the same total. */
+__device__ __forceinline__ float wave_sum(float v) {
+    float a[1] = {v};
+    return wave_sum_rows<1>(a, 0);
 }
 
 __device__ __forceinline__ double wave_sum(double v) {
@@ -160,11 +204,8 @@ __device__ __forceinline__ void group16(const char* W, g_u32x4* x, g_f32* y, int
 #pragma unroll
             for (int u = 0; u < U; ++u) acc[r] = dot8<FMT>(wv[r][u], xv[u], acc[r]);
     }
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const float s = wave_sum(acc[r]);
-        if (lane == 0) y[i + r] = s;
-    }
+    const float s = wave_sum_rows<R>(acc, lane);
+    if ((lane & (WAVE / R - 1)) == 0) y[i + lane / (WAVE / R)] = s;
 }
 
 /* Rows [r0, r1) of matrix d at token `token` (r0, r1 wave-uniform): groups of R rows, then the
@@ -306,12 +347,10 @@ __device__ __forceinline__ void q4_compute(const Q4Step<R, U>& st, float (&acc)[
 
 template <int R>
 __device__ __forceinline__ void q4_store(g_f32* y, int64_t i, float (&acc)[R], int lane) {
+    const float s = wave_sum_rows<R>(acc, lane) * 16777216.0f;   /* undo the 2^-24 unit (exact) */
+    if ((lane & (WAVE / R - 1)) == 0) y[i + lane / (WAVE / R)] = s;
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const float s = wave_sum(acc[r]) * 16777216.0f;   /* undo the 2^-24 unit (exact) */
-        if (lane == 0) y[i + r] = s;
-        acc[r] = 0.f;
-    }
+    for (int r = 0; r < R; ++r) acc[r] = 0.f;
 }
 
 /* Rows [i, i + R), any block count: one step at a time. */
@@ -337,12 +376,12 @@ __device__ __forceinline__ void q4_group(g_u32x4* Wq, g_u16* S, g_u32x4* x, g_f3
     q4_store<R>(y, i, acc, lane);
 }
 
-/* Rows [r0, r1) of a q4 matrix.  When rows hold whole steps (nb a multiple of 64 U) the groups of
-   R rows run as one software pipeline: the loads of the next step (of this row group or the
+/* Rows [r0, r1) of a q4 matrix.  With PIPE, when rows hold whole steps (nb a multiple of 64 U), the
+   groups of R rows run as one software pipeline: the loads of the next step (of this row group or the
    next one) are issued before the current step is decoded, two register sets taking turns, so
    every wave keeps memory requests in flight while it computes.  Remaining rows go one at a
    time. */
-template <int R, int U>
+template <int R, int U, bool PIPE = true>
 __device__ __forceinline__ void rows_q4(const DevMat& d, int64_t r0, int64_t r1, int32_t token,
                                         int lane) {
     g_u32x4* Wq = as_global<g_u32x4*>(d.w);
@@ -353,7 +392,9 @@ __device__ __forceinline__ void rows_q4(const DevMat& d, int64_t r0, int64_t r1,
     constexpr int STEP = WAVE * U;
     const int64_t ngroups = (r1 - r0) / R;
     int64_t i_end = r0 + ngroups * R;
-    if (ngroups > 0 && nb % STEP == 0 && nb > 0) {
+    if (!PIPE) {
+        for (int64_t i = r0; i < i_end; i += R) q4_group<R, U>(Wq, S, x, y, nb, i, lane);
+    } else if (ngroups > 0 && nb % STEP == 0 && nb > 0) {
         const int64_t steps = nb / STEP;                 /* steps per row group */
         g_u32x4* wr[R];
         g_u16* sr[R];
@@ -405,7 +446,7 @@ __device__ __forceinline__ void rows_q4(const DevMat& d, int64_t r0, int64_t r1,
    same wave, so increasing ranges resume where the last one ended. */
 __device__ __forceinline__ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-template <int FMT, int R16, int U16, int RQ, int UQ>
+template <int FMT, int R16, int U16, int RQ, int UQ, bool QPIPE = true>
 __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, int nmat, int64_t lo,
                                              int64_t hi, int32_t token, int lane, int& hint) {
     int a = hint;
@@ -430,7 +471,7 @@ __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, int
         else if ((FMT == 0 || FMT == FMT_BF16) && fmt == FMT_BF16)
             rows16<FMT_BF16, R16, U16>(d, r0, r1, token, lane);
         else if ((FMT == 0 || FMT == FMT_Q4) && fmt == FMT_Q4)
-            rows_q4<RQ, UQ>(d, r0, r1, token, lane);
+            rows_q4<RQ, UQ, QPIPE>(d, r0, r1, token, lane);
     }
 }
 

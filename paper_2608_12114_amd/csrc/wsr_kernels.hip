@@ -192,14 +192,14 @@ hipError_t launch_put_table(DevMat* dst, const DevMat* src, int n, unsigned* ctr
    Every row has exactly one owner either way, and its result does not depend on the owner. */
 enum : int { SCHED_TILES = 0, SCHED_SPANS = 1 };
 
-/* Tile size: about four tiles per wave, a power of two between 64 KiB and 1 MiB. */
+/* Tile size: about four tiles per wave, a power of two between 64 KiB and 2 MiB. */
 int64_t sweep_tile(int64_t total, int64_t waves) {
     int64_t t = 64 << 10;
-    while (t < (1 << 20) && t * waves * 4 < total) t <<= 1;
+    while (t < (2 << 20) && t * waves * 4 < total) t <<= 1;
     return t;
 }
 
-template <int FMT, int SCHED, int R16, int U16, int RQ, int UQ>
+template <int FMT, int SCHED, int R16, int U16, int RQ, int UQ, bool QPIPE = true>
 __global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab, int nmat, int64_t total,
                                                  int64_t tile, int32_t token, unsigned* __restrict__ ctr) {
     const int lane = threadIdx.x & (WAVE - 1);
@@ -208,7 +208,7 @@ __global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab,
     if constexpr (SCHED == SCHED_SPANS) {
         const int64_t w = (int64_t)blockIdx.x * WAVES_PER_BLOCK + wave_in_block();
         const int64_t lo = total * w / nw, hi = total * (w + 1) / nw;
-        if (lo < hi) stream_range<FMT, R16, U16, RQ, UQ>(tab, nmat, lo, hi, token, lane, hint);
+        if (lo < hi) stream_range<FMT, R16, U16, RQ, UQ, QPIPE>(tab, nmat, lo, hi, token, lane, hint);
     } else {
         const int64_t ntiles = ceil_div(total, tile);
         for (;;) {
@@ -217,8 +217,8 @@ __global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab,
             t = __builtin_amdgcn_readfirstlane(t);
             if ((int64_t)t >= ntiles) break;
             const int64_t lo = (int64_t)t * tile;
-            stream_range<FMT, R16, U16, RQ, UQ>(tab, nmat, lo, std::min<int64_t>(total, lo + tile), token,
-                                                lane, hint);
+            stream_range<FMT, R16, U16, RQ, UQ, QPIPE>(tab, nmat, lo, std::min<int64_t>(total, lo + tile),
+                                                       token, lane, hint);
         }
         if (lane == 0) {
             const unsigned e = __hip_atomic_fetch_add(ctr + 1, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
@@ -243,10 +243,10 @@ static int cu_count() {
     return cache[dev];
 }
 
-/* 16-bit weights: tiles, 4 rows x 4 KiB steps per wave, two blocks per CU (few, long streams);
+/* 16-bit weights: tiles, 4 rows x 4 KiB steps per wave, one block (4 waves) per CU (few, long streams);
    q4: spans, 8 rows x 1 block per lane per step (eight rows share each block's activation
    decode), software-pipelined. */
-constexpr int SWEEP_BLOCKS_PER_CU_16 = 2;
+constexpr int SWEEP_BLOCKS_PER_CU_16 = 1;
 constexpr int SWEEP_BLOCKS_PER_CU_Q4 = 4;
 
 hipError_t launch_sweep(const DevMat* tab, int nmat, int64_t total, int fmt_all, int32_t token,

@@ -95,3 +95,33 @@ def test_sweep_ragged_shapes(layers, d, ffn, fmt):
     for i in range(len(mats)):
         for t in range(2):
             assert rel_l2(ys[i][t], oracle_y(inp, i, t)) <= TOL, (i, t)
+
+
+def _check_sampled(inp, tokens, nrows=6):
+    """Sampled rows (first, last, spread) of every matrix against the oracle, row by row."""
+    worst = 0.0
+    for i, m in enumerate(inp.mats):
+        rows = np.unique(np.linspace(0, m.M - 1, nrows).astype(np.int64))
+        ys = inp.y[i][tokens].cpu().numpy()
+        for t_i, t in enumerate(tokens):
+            got = ys[t_i][rows]
+            want = oracle_y(inp, i, t, rows)
+            err = rel_l2(got, want)
+            assert err <= TOL, (m.layer, m.name, t, err)
+            worst = max(worst, err)
+    return worst
+
+
+@pytest.mark.parametrize("name", ["llama3-8b-q4", "llama-70b-bf16"])
+def test_sweep_full_size(name):
+    """The decode sweeps at their full shapes, in the launch configuration bench.py times: every
+    matrix checked on sampled rows for the first and last of four tokens."""
+    _, shape, fmt = {"llama3-8b-q4": wl.LLAMA8B_Q4, "llama-70b-bf16": wl.LLAMA70B_BF16}[name]
+    mats = wl.decode_matrices(shape)
+    inp = dv.SweepInputs(mats, [fmt] * len(mats), tokens=4)
+    assert inp.weight_bytes() == wl.bytes_per_token(shape, fmt)
+    ys = run_sweep(inp, 4)
+    del ys
+    _check_sampled(inp, [0, 3])
+    del inp
+    torch.cuda.empty_cache()
