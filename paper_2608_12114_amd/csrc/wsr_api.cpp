@@ -214,7 +214,8 @@ wsr_status wsr_gemv_q4(const uint8_t* Wq, const uint16_t* scales, const uint16_t
 size_t wsr_sweep_workspace_bytes(const wsr_mat* mats, int32_t n) {
     (void)mats;
     if (n <= 0) return 0;
-    return wsr::SWEEP_CTR_BYTES + ((size_t)n * sizeof(DevMat) + 255) / 256 * 256;
+    return wsr::SWEEP_CTR_BYTES + ((size_t)n * sizeof(DevMat) + 255) / 256 * 256 +
+           ((size_t)n * sizeof(int64_t) + 255) / 256 * 256;
 }
 
 wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, void* ws,
@@ -256,11 +257,13 @@ wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, vo
     hipStream_t s = static_cast<hipStream_t>(stream);
     unsigned* ctr = static_cast<unsigned*>(ws);
     DevMat* dtab = reinterpret_cast<DevMat*>(static_cast<char*>(ws) + wsr::SWEEP_CTR_BYTES);
-    hipError_t e = wsr::launch_put_table(dtab, tab.data(), n, ctr, s);
+    int64_t* dcost = reinterpret_cast<int64_t*>(reinterpret_cast<char*>(dtab) +
+                                                ((size_t)n * sizeof(DevMat) + 255) / 256 * 256);
+    hipError_t e = wsr::launch_put_table(dtab, dcost, tab.data(), n, ctr, s);
     if (e != hipSuccess) return hip_fail(e, "decode_sweep: table upload");
     for (int32_t t = 0; t < n_tokens; ++t)
         for (const Seg& g : segs) {
-            e = wsr::launch_sweep(dtab + g.first, g.count, g.total, g.fmt, t, ctr, s);
+            e = wsr::launch_sweep(dtab + g.first, dcost + g.first, g.count, g.total, g.fmt, t, ctr, s);
             if (e != hipSuccess) return hip_fail(e, "decode_sweep: launch");
         }
     return ok();

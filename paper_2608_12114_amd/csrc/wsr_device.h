@@ -376,12 +376,12 @@ __device__ __forceinline__ void q4_group(g_u32x4* Wq, g_u16* S, g_u32x4* x, g_f3
     q4_store<R>(y, i, acc, lane);
 }
 
-/* Rows [r0, r1) of a q4 matrix.  With PIPE, when rows hold whole steps (nb a multiple of 64 U), the
-   groups of R rows run as one software pipeline: the loads of the next step (of this row group or the
-   next one) are issued before the current step is decoded, two register sets taking turns, so
-   every wave keeps memory requests in flight while it computes.  Remaining rows go one at a
-   time. */
-template <int R, int U, bool PIPE = true>
+/* Rows [r0, r1) of a q4 matrix.  With NB >= 2, when rows hold whole steps (nb a multiple of 64 U),
+   the units (group of R rows, step) run as one software pipeline over NB register sets: the loads
+   of the NB - 1 units after the current one are in flight while it is decoded.  The main loop is
+   unrolled by NB so every set is named statically and its loads are unconditional, which keeps
+   the waits exact; the last units are decoded after it.  Remaining rows go one at a time. */
+template <int R, int U, int NB = 2>
 __device__ __forceinline__ void rows_q4(const DevMat& d, int64_t r0, int64_t r1, int32_t token,
                                         int lane) {
     g_u32x4* Wq = as_global<g_u32x4*>(d.w);
@@ -392,46 +392,52 @@ __device__ __forceinline__ void rows_q4(const DevMat& d, int64_t r0, int64_t r1,
     constexpr int STEP = WAVE * U;
     const int64_t ngroups = (r1 - r0) / R;
     int64_t i_end = r0 + ngroups * R;
-    if (!PIPE) {
+    if (NB < 2) {
         for (int64_t i = r0; i < i_end; i += R) q4_group<R, U>(Wq, S, x, y, nb, i, lane);
     } else if (ngroups > 0 && nb % STEP == 0 && nb > 0) {
         const int64_t steps = nb / STEP;                 /* steps per row group */
-        g_u32x4* wr[R];
-        g_u16* sr[R];
-        auto point = [&](int64_t g) {                    /* row pointers of group g */
-            const int64_t i = r0 + g * R;
+        const int64_t n = ngroups * steps;               /* units */
+        float acc[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) acc[r] = 0.f;
+        int64_t gl = 0, kl = 0;                          /* next unit to load    */
+        int64_t gc = 0, kc = 0;                          /* next unit to decode  */
+        auto load = [&](Q4Step<R, U>& st) {
+            g_u32x4* wr[R];
+            g_u16* sr[R];
+            const int64_t i = r0 + gl * R;
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 wr[r] = Wq + (i + r) * nb;
                 sr[r] = S + (i + r) * nb;
             }
+            q4_load<R, U>(st, wr, sr, x, kl * STEP, lane);
+            if (++kl == steps) { kl = 0; ++gl; }
         };
-        float acc[R];
+        auto decode = [&](const Q4Step<R, U>& st) {
+            q4_compute<R, U>(st, acc);
+            if (kc + 1 == steps) q4_store<R>(y, r0 + gc * R, acc, lane);
+            if (++kc == steps) { kc = 0; ++gc; }
+        };
+        Q4Step<R, U> buf[NB];
 #pragma unroll
-        for (int r = 0; r < R; ++r) acc[r] = 0.f;
-        Q4Step<R, U> A, B;
-        int64_t g = 0, k = 0;                            /* (group, step) of the unit in A */
-        point(0);
-        q4_load<R, U>(A, wr, sr, x, 0, lane);
-        for (;;) {
-            int64_t g1 = g, k1 = k + 1;
-            if (k1 == steps) { k1 = 0; ++g1; }
-            bool more = g1 < ngroups;
-            if (more) { point(g1); q4_load<R, U>(B, wr, sr, x, k1 * STEP, lane); }
-            __builtin_amdgcn_sched_barrier(0);           /* keep those loads ahead of the decode */
-            q4_compute<R, U>(A, acc);
-            if (k + 1 == steps) q4_store<R>(y, r0 + g * R, acc, lane);
-            if (!more) break;
-            g = g1; k = k1;                              /* the unit in B */
-            g1 = g; k1 = k + 1;
-            if (k1 == steps) { k1 = 0; ++g1; }
-            more = g1 < ngroups;
-            if (more) { point(g1); q4_load<R, U>(A, wr, sr, x, k1 * STEP, lane); }
-            __builtin_amdgcn_sched_barrier(0);
-            q4_compute<R, U>(B, acc);
-            if (k + 1 == steps) q4_store<R>(y, r0 + g * R, acc, lane);
-            if (!more) break;
-            g = g1; k = k1;                              /* the unit in A */
+        for (int j = 0; j < NB - 1; ++j)
+            if (j < n) load(buf[j]);
+        int64_t u = 0;                                   /* buf[j] holds unit u + j, j < NB - 1 */
+        for (; u + 2 * NB - 1 <= n; u += NB) {
+#pragma unroll
+            for (int j = 0; j < NB; ++j) {
+                load(buf[(j + NB - 1) % NB]);            /* unit u + j + NB - 1 */
+                __builtin_amdgcn_sched_barrier(0);       /* keep those loads ahead of the decode */
+                decode(buf[j]);                          /* unit u + j */
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 2 * NB - 1; ++j) {
+            if (u + j < n) {
+                if (u + j + NB - 1 < n) load(buf[(j + NB - 1) % NB]);
+                decode(buf[j % NB]);
+            }
         }
     } else {
         i_end = r0;
@@ -439,39 +445,42 @@ __device__ __forceinline__ void rows_q4(const DevMat& d, int64_t r0, int64_t r1,
     for (int64_t i = i_end; i < r1; ++i) q4_group<1, U>(Wq, S, x, y, nb, i, lane);
 }
 
-/* ---- ranges of the weight stream ---------------------------------------------------------------
-
-   The rows of a table of matrices, in table order, form one weight stream; a row belongs to the byte
-   range that holds its first byte.  `hint` carries the matrix index of the previous range of the
-   same wave, so increasing ranges resume where the last one ended. */
 __device__ __forceinline__ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-template <int FMT, int R16, int U16, int RQ, int UQ, bool QPIPE = true>
-__device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, int nmat, int64_t lo,
-                                             int64_t hi, int32_t token, int lane, int& hint) {
+template <int FMT, int R16, int U16, int RQ, int UQ, int QNB = 2>
+__device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, const int64_t* __restrict__ cost,
+                                             int nmat, int64_t lo, int64_t hi, int32_t token, int lane,
+                                             int& hint) {
+    /* Last matrix whose stream starts at or before lo: from the hint when it still holds, else by
+       bisection over the dense offset array (8 bytes per matrix, so it stays in the scalar cache). */
     int a = hint;
-    if (tab[a].cost0 > lo) a = 0;
-    if (a + 1 < nmat && tab[a + 1].cost0 <= lo) {   /* last matrix whose stream starts <= lo */
+    if (cost[a] > lo) a = 0;
+    if (a + 1 < nmat && cost[a + 1] <= lo) {
         int b = nmat - 1;
         while (a < b) {
             const int mid = (a + b + 1) >> 1;
-            if (tab[mid].cost0 <= lo) a = mid; else b = mid - 1;
+            if (cost[mid] <= lo) a = mid; else b = mid - 1;
         }
     }
     for (int m = a; m < nmat; ++m) {
         const DevMat d = tab[m];
         if (d.cost0 >= hi) break;
         hint = m;
-        const int64_t r0 = lo > d.cost0 ? ceil_div(lo - d.cost0, d.row_bytes) : 0;
-        const int64_t r1 = d.M < ceil_div(hi - d.cost0, d.row_bytes) ? d.M : ceil_div(hi - d.cost0, d.row_bytes);
-        if (r0 >= r1) continue;
         const int fmt = FMT ? FMT : d.fmt;
+        /* A byte boundary maps to the first row group starting at or after it, the same way for
+           the ranges on both sides, so the ranges still cover each row once and break only
+           between whole groups of R rows. */
+        const int64_t g = fmt == FMT_Q4 ? RQ : R16;
+        const int64_t r0 = lo > d.cost0 ? ceil_div(lo - d.cost0, d.row_bytes * g) * g : 0;
+        const int64_t e1 = ceil_div(hi - d.cost0, d.row_bytes * g) * g;
+        const int64_t r1 = d.M < e1 ? d.M : e1;
+        if (r0 >= r1) continue;
         if ((FMT == 0 || FMT == FMT_F16) && fmt == FMT_F16)
             rows16<FMT_F16, R16, U16>(d, r0, r1, token, lane);
         else if ((FMT == 0 || FMT == FMT_BF16) && fmt == FMT_BF16)
             rows16<FMT_BF16, R16, U16>(d, r0, r1, token, lane);
         else if ((FMT == 0 || FMT == FMT_Q4) && fmt == FMT_Q4)
-            rows_q4<RQ, UQ, QPIPE>(d, r0, r1, token, lane);
+            rows_q4<RQ, UQ, QNB>(d, r0, r1, token, lane);
     }
 }
 

@@ -36,11 +36,13 @@ int64_t probe_grid(int64_t n);
 
 hipError_t launch_gemv(const DevMat& m, hipStream_t s);
 /* Writes the table and clears the two tile counters at ctr (ctr may be null). */
-hipError_t launch_put_table(DevMat* dst, const DevMat* src, int n, unsigned* ctr, hipStream_t s);
-hipError_t launch_sweep(const DevMat* tab, int nmat, int64_t total_bytes, int fmt_all,
-                        int32_t token, unsigned* ctr, hipStream_t s);
+hipError_t launch_put_table(DevMat* dst, int64_t* cost, const DevMat* src, int n, unsigned* ctr,
+                            hipStream_t s);
+hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, int nmat, int64_t total_bytes,
+                        int fmt_all, int32_t token, unsigned* ctr, hipStream_t s);
 
-/* Sweep workspace: tile counters in the first SWEEP_CTR_BYTES, then the table. */
+/* Sweep workspace: tile counters in the first SWEEP_CTR_BYTES, then the table, then the matrices'
+   stream offsets (DevMat::cost0) as a dense int64 array, each part padded to 256 bytes. */
 constexpr size_t SWEEP_CTR_BYTES = 256;
 
 }  // namespace wsr

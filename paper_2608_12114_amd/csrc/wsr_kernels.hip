@@ -166,31 +166,31 @@ struct TableChunk {
     DevMat m[TABLE_CHUNK];
 };
 
-__global__ __launch_bounds__(WAVE) void k_put_table(DevMat* __restrict__ dst, TableChunk c,
-                                                    unsigned* __restrict__ ctr) {
+__global__ __launch_bounds__(WAVE) void k_put_table(DevMat* __restrict__ dst, int64_t* __restrict__ cost,
+                                                    TableChunk c, unsigned* __restrict__ ctr) {
     const int i = threadIdx.x;
-    if (i < c.n) dst[i] = c.m[i];
+    if (i < c.n) {
+        dst[i] = c.m[i];
+        cost[i] = c.m[i].cost0;
+    }
     if (ctr && i < 2) ctr[i] = 0u;
 }
 
-hipError_t launch_put_table(DevMat* dst, const DevMat* src, int n, unsigned* ctr, hipStream_t s) {
+hipError_t launch_put_table(DevMat* dst, int64_t* cost, const DevMat* src, int n, unsigned* ctr,
+                            hipStream_t s) {
     for (int first = 0; first < n; first += TABLE_CHUNK) {
         TableChunk c{};
         c.n = std::min(TABLE_CHUNK, n - first);
         for (int i = 0; i < c.n; ++i) c.m[i] = src[first + i];
-        hipLaunchKernelGGL(k_put_table, dim3(1), dim3(WAVE), 0, s, dst + first, c, first == 0 ? ctr : nullptr);
+        hipLaunchKernelGGL(k_put_table, dim3(1), dim3(WAVE), 0, s, dst + first, cost + first, c,
+                           first == 0 ? ctr : nullptr);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
 }
 
-/* Schedules over the weight stream of one launch (`total` bytes):
-   TILES  waves take tiles of `tile` bytes in order from a counter (ctr[0]); a wave that finds none
-          left checks out on ctr[1], and the last one resets both for the next launch.
-   SPANS  wave w of nw owns [w * total / nw, (w + 1) * total / nw) (no counters).
-   Every row has exactly one owner either way, and its result does not depend on the owner. */
-enum : int { SCHED_TILES = 0, SCHED_SPANS = 1 };
+enum : int { SCHED_TILES = 0, SCHED_SPANS = 1, SCHED_HYBRID = 2 };
 
 /* Tile size: about four tiles per wave, a power of two between 64 KiB and 2 MiB. */
 int64_t sweep_tile(int64_t total, int64_t waves) {
@@ -199,26 +199,44 @@ int64_t sweep_tile(int64_t total, int64_t waves) {
     return t;
 }
 
-template <int FMT, int SCHED, int R16, int U16, int RQ, int UQ, bool QPIPE = true>
-__global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab, int nmat, int64_t total,
-                                                 int64_t tile, int32_t token, unsigned* __restrict__ ctr) {
+/* Work distribution over the weight stream [0, total) of one token:
+     SCHED_TILES   tiles of `tile` bytes, claimed in order from a counter;
+     SCHED_SPANS   wave w takes [total w / nw, total (w + 1) / nw);
+     SCHED_HYBRID  wave w first takes [span w, span (w + 1)), then the rest [span nw, total) goes out
+                   in claimed tiles, so long uninterrupted runs carry most of the stream and the
+                   waves that finish early share the remainder.
+   The counters ctr[0] (next tile) and ctr[1] (waves done) start at zero and the last wave to
+   finish puts them back to zero for the next launch. */
+template <int FMT, int SCHED, int R16, int U16, int RQ, int UQ, int QNB = 2>
+__global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab, const int64_t* __restrict__ cost,
+                                                 int nmat, int64_t total, int64_t span, int64_t tile,
+                                                 int32_t token, unsigned* __restrict__ ctr) {
     const int lane = threadIdx.x & (WAVE - 1);
     const unsigned nw = gridDim.x * WAVES_PER_BLOCK;
+    const int64_t w = (int64_t)blockIdx.x * WAVES_PER_BLOCK + wave_in_block();
     int hint = 0;
     if constexpr (SCHED == SCHED_SPANS) {
-        const int64_t w = (int64_t)blockIdx.x * WAVES_PER_BLOCK + wave_in_block();
         const int64_t lo = total * w / nw, hi = total * (w + 1) / nw;
-        if (lo < hi) stream_range<FMT, R16, U16, RQ, UQ, QPIPE>(tab, nmat, lo, hi, token, lane, hint);
+        if (lo < hi) stream_range<FMT, R16, U16, RQ, UQ, QNB>(tab, cost, nmat, lo, hi, token, lane, hint);
     } else {
-        const int64_t ntiles = ceil_div(total, tile);
+        int64_t base = 0;
+        if constexpr (SCHED == SCHED_HYBRID) {
+            base = span * nw;
+            if (span > 0) stream_range<FMT, R16, U16, RQ, UQ, QNB>(tab, cost, nmat, span * w, span * (w + 1),
+                                                                   token, lane, hint);
+        }
+        /* Each wave claims its next tile before working on the current one, so the round trip of
+           the claim overlaps the current tile's loads. */
+        const int64_t ntiles = ceil_div(total - base, tile);
+        unsigned claim = 0;
+        if (lane == 0) claim = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         for (;;) {
-            unsigned t = 0;
-            if (lane == 0) t = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            t = __builtin_amdgcn_readfirstlane(t);
+            const unsigned t = __builtin_amdgcn_readfirstlane(claim);
             if ((int64_t)t >= ntiles) break;
-            const int64_t lo = (int64_t)t * tile;
-            stream_range<FMT, R16, U16, RQ, UQ, QPIPE>(tab, nmat, lo, std::min<int64_t>(total, lo + tile),
-                                                       token, lane, hint);
+            if (lane == 0) claim = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const int64_t lo = base + (int64_t)t * tile;
+            stream_range<FMT, R16, U16, RQ, UQ, QNB>(tab, cost, nmat, lo, std::min<int64_t>(total, lo + tile),
+                                                     token, lane, hint);
         }
         if (lane == 0) {
             const unsigned e = __hip_atomic_fetch_add(ctr + 1, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
@@ -249,24 +267,24 @@ static int cu_count() {
 constexpr int SWEEP_BLOCKS_PER_CU_16 = 1;
 constexpr int SWEEP_BLOCKS_PER_CU_Q4 = 4;
 
-hipError_t launch_sweep(const DevMat* tab, int nmat, int64_t total, int fmt_all, int32_t token,
-                        unsigned* ctr, hipStream_t s) {
+hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, int nmat, int64_t total, int fmt_all,
+                        int32_t token, unsigned* ctr, hipStream_t s) {
     if (nmat == 0 || total == 0) return hipSuccess;
     const int bpc = fmt_all == FMT_Q4 ? SWEEP_BLOCKS_PER_CU_Q4 : SWEEP_BLOCKS_PER_CU_16;
     const dim3 grid((unsigned)(cu_count() * bpc)), block(BLOCK);
     const int64_t tile = sweep_tile(total, (int64_t)grid.x * WAVES_PER_BLOCK);
     switch (fmt_all) {
         case FMT_F16:
-            hipLaunchKernelGGL((k_sweep<FMT_F16, SCHED_TILES, 4, 4, 8, 1>), grid, block, 0, s, tab, nmat, total, tile, token, ctr);
+            hipLaunchKernelGGL((k_sweep<FMT_F16, SCHED_TILES, 4, 4, 8, 1>), grid, block, 0, s, tab, cost, nmat, total, (int64_t)0, tile, token, ctr);
             break;
         case FMT_BF16:
-            hipLaunchKernelGGL((k_sweep<FMT_BF16, SCHED_TILES, 4, 4, 8, 1>), grid, block, 0, s, tab, nmat, total, tile, token, ctr);
+            hipLaunchKernelGGL((k_sweep<FMT_BF16, SCHED_TILES, 4, 4, 8, 1>), grid, block, 0, s, tab, cost, nmat, total, (int64_t)0, tile, token, ctr);
             break;
         case FMT_Q4:
-            hipLaunchKernelGGL((k_sweep<FMT_Q4, SCHED_SPANS, 4, 4, 8, 1>), grid, block, 0, s, tab, nmat, total, tile, token, ctr);
+            hipLaunchKernelGGL((k_sweep<FMT_Q4, SCHED_SPANS, 4, 4, 8, 1>), grid, block, 0, s, tab, cost, nmat, total, (int64_t)0, tile, token, ctr);
             break;
         default:
-            hipLaunchKernelGGL((k_sweep<0, SCHED_TILES, 4, 4, 8, 1>), grid, block, 0, s, tab, nmat, total, tile, token, ctr);
+            hipLaunchKernelGGL((k_sweep<0, SCHED_TILES, 4, 4, 8, 1>), grid, block, 0, s, tab, cost, nmat, total, (int64_t)0, tile, token, ctr);
             break;
     }
     return hipGetLastError();

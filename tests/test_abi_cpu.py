@@ -79,7 +79,7 @@ def test_sweep_argument_checks():
     good = dict(fmt=2, M=8, K=64, w=A, x=A, y=A, x_tok_stride=128, y_tok_stride=32)
     mats = wsr.make_mats([good, dict(good, fmt=3, scales=A)])
     ws = wsr.wsr_sweep_workspace_bytes(mats)
-    assert ws == 256 + 256
+    assert ws == 256 + 256 + 256        # counters, table, stream offsets
     f = "wsr_decode_sweep"
     assert _status(f, mats, 2, 0, A, ws, None) == wsr.WSR_E_ARG             # n_tokens < 1
     assert _status(f, mats, 2, 1, A + 16, ws, None) == wsr.WSR_E_ALIGN      # ws 256-byte alignment
