@@ -133,7 +133,8 @@ wsr_status wsr_gemv_q4(const uint8_t* Wq, const uint16_t* scales, const uint16_t
    Matrices of one token run in one persistent launch unless a matrix has WSR_MAT_AFTER_PREVIOUS,
    which starts a new launch so that it may read outputs of earlier matrices of the same token.
    ws: at least wsr_sweep_workspace_bytes(mats, n) bytes of device memory, 256-byte aligned; each
-   call writes the matrix table and the launches' work counters there (no initialisation needed). */
+   call writes the launches' work counters, the matrix table and the matrices' stream offsets
+   there (no initialisation needed). */
 #define WSR_MAT_AFTER_PREVIOUS 1
 typedef struct wsr_mat {
     int32_t fmt;            /* wsr_fmt                                                    */

@@ -15,8 +15,10 @@ ARCH = "gfx950"
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", f"-I{INCLUDE}", f"-I{CSRC}"]
 # Packed fp32 instructions are kept out of every kernel (the host pass warns it does not know the
 # feature; that is expected).
+# The atomic optimizer turns a single-lane atomic with a return value into a wave-wide scan that
+# consumes the result at once; the sweep's tile claims are issued ahead of use and must stay plain.
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-          "-ffp-contract=fast"]
+          "-ffp-contract=fast", "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]
 
 
 def _run(cmd):

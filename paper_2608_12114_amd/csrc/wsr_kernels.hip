@@ -9,9 +9,11 @@
  *              and clears the sweep's tile counters, so a sweep needs no host copy or host
  *              synchronisation (C3, Table 1)
  *
- * Streaming layout.  HBM3E serves long sequential runs best: each probe block walks its own
- * contiguous region, and the sweep hands out 1 MiB tiles of the weight stream in order, so the
- * waves in flight all work on one moving front of memory.
+ * Streaming layout.  HBM3E serves long sequential runs best.  Each probe block walks its own
+ * contiguous region.  The 16-bit sweep hands out tiles of the weight stream (64 KiB to 2 MiB) in
+ * order from a counter, so the waves in flight work on one moving front of memory and finish
+ * together.  The q4 sweep gives each wave an equal contiguous span instead, which measured faster
+ * for its heavier per-byte work; its waves keep several steps of loads in flight in registers.
  */
 #include <hip/hip_runtime.h>
 
@@ -146,9 +148,9 @@ hipError_t launch_gemv(const DevMat& m, hipStream_t s) {
     if (m.M == 0) return hipSuccess;
     switch (m.fmt) {
         case FMT_F16:
-            return launch_rows(k_gemv16<FMT_F16, 1, 4>, m, 1, s);
+            return launch_rows(k_gemv16<FMT_F16, 1, 8>, m, 1, s);
         case FMT_BF16:
-            return launch_rows(k_gemv16<FMT_BF16, 1, 4>, m, 1, s);
+            return launch_rows(k_gemv16<FMT_BF16, 1, 8>, m, 1, s);
         case FMT_Q4:
             return m.nc >= 256 ? launch_rows(k_gemv_q4<2, 2>, m, 2, s)
                                : launch_rows(k_gemv_q4<4, 1>, m, 4, s);
