@@ -203,7 +203,9 @@ int64_t sweep_tile(int64_t total, int64_t waves) {
 
 /* Work distribution over the weight stream [0, total) of one token:
      SCHED_TILES   tiles of `tile` bytes, claimed in order from a counter;
-     SCHED_SPANS   wave w takes [total w / nw, total (w + 1) / nw);
+     SCHED_SPANS   wave w takes [total w / nw, total (w + 1) / nw); with many more blocks than the
+                   chip holds at once, the hardware starts each block as an earlier one retires,
+                   which balances the end of the token at no cost;
      SCHED_HYBRID  wave w first takes [span w, span (w + 1)), then the rest [span nw, total) goes out
                    in claimed tiles, so long uninterrupted runs carry most of the stream and the
                    waves that finish early share the remainder.
@@ -218,7 +220,10 @@ __global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab,
     const int64_t w = (int64_t)blockIdx.x * WAVES_PER_BLOCK + wave_in_block();
     int hint = 0;
     if constexpr (SCHED == SCHED_SPANS) {
-        const int64_t lo = total * w / nw, hi = total * (w + 1) / nw;
+        /* floor(total w / nw) without forming total * w */
+        const int64_t q = total / nw, r = total % nw;
+        const int64_t lo = q * w + (int64_t)((uint64_t)r * (uint64_t)w / nw);
+        const int64_t hi = q * (w + 1) + (int64_t)((uint64_t)r * (uint64_t)(w + 1) / nw);
         if (lo < hi) stream_range<FMT, R16, U16, RQ, UQ, QNB>(tab, cost, nmat, lo, hi, token, lane, hint);
     } else {
         int64_t base = 0;
@@ -263,17 +268,28 @@ static int cu_count() {
     return cache[dev];
 }
 
-/* 16-bit weights: tiles, 4 rows x 4 KiB steps per wave, one block (4 waves) per CU (few, long streams);
-   q4: spans, 8 rows x 1 block per lane per step (eight rows share each block's activation
-   decode), software-pipelined. */
+/* 16-bit weights: tiles, 4 rows x 4 KiB steps per wave, one block (4 waves) per CU (few, long
+   streams).  q4: spans of about 64 KiB per wave, 8 rows x 1 block per lane per step (eight rows
+   share each block's activation decode), two register sets in flight; the grid is sized so that
+   blocks retire and are replaced throughout the token (16,100 blocks for 4.2 GB). */
 constexpr int SWEEP_BLOCKS_PER_CU_16 = 1;
-constexpr int SWEEP_BLOCKS_PER_CU_Q4 = 4;
+constexpr int64_t SWEEP_SPAN_Q4 = 64 << 10;
 
 hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, int nmat, int64_t total, int fmt_all,
                         int32_t token, unsigned* ctr, hipStream_t s) {
     if (nmat == 0 || total == 0) return hipSuccess;
-    const int bpc = fmt_all == FMT_Q4 ? SWEEP_BLOCKS_PER_CU_Q4 : SWEEP_BLOCKS_PER_CU_16;
-    const dim3 grid((unsigned)(cu_count() * bpc)), block(BLOCK);
+    const dim3 block(BLOCK);
+    if (fmt_all == FMT_Q4) {
+        /* About SWEEP_SPAN_Q4 bytes per wave, at least one wave per SIMD. */
+        const int64_t waves = std::max<int64_t>((int64_t)cu_count() * WAVES_PER_BLOCK,
+                                                (total + SWEEP_SPAN_Q4 - 1) / SWEEP_SPAN_Q4);
+        const int64_t blocks = (waves + WAVES_PER_BLOCK - 1) / WAVES_PER_BLOCK;
+        if (blocks > INT32_MAX) return hipErrorInvalidValue;
+        hipLaunchKernelGGL((k_sweep<FMT_Q4, SCHED_SPANS, 4, 4, 8, 1>), dim3((unsigned)blocks), block, 0, s, tab, cost,
+                           nmat, total, (int64_t)0, (int64_t)0, token, ctr);
+        return hipGetLastError();
+    }
+    const dim3 grid((unsigned)(cu_count() * SWEEP_BLOCKS_PER_CU_16));
     const int64_t tile = sweep_tile(total, (int64_t)grid.x * WAVES_PER_BLOCK);
     switch (fmt_all) {
         case FMT_F16:
@@ -281,9 +297,6 @@ hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, int nmat, int64_
             break;
         case FMT_BF16:
             hipLaunchKernelGGL((k_sweep<FMT_BF16, SCHED_TILES, 4, 4, 8, 1>), grid, block, 0, s, tab, cost, nmat, total, (int64_t)0, tile, token, ctr);
-            break;
-        case FMT_Q4:
-            hipLaunchKernelGGL((k_sweep<FMT_Q4, SCHED_SPANS, 4, 4, 8, 1>), grid, block, 0, s, tab, cost, nmat, total, (int64_t)0, tile, token, ctr);
             break;
         default:
             hipLaunchKernelGGL((k_sweep<0, SCHED_TILES, 4, 4, 8, 1>), grid, block, 0, s, tab, cost, nmat, total, (int64_t)0, tile, token, ctr);
