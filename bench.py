@@ -71,6 +71,10 @@ def parse():
                    help="comma list of extra rows ('' for none)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time of the sample")
+    p.add_argument("--passes", type=int, default=4, help="extra timed passes for the spread")
+    p.add_argument("--processes", type=int, default=0,
+                   help="run the headline in this many child processes, one after another, and report "
+                        "the median of their medians (a separate JSON line; no GPU use in this process)")
     return p.parse_args()
 
 
@@ -115,7 +119,18 @@ def sweep_workload(name, tokens_needed, stream, wsr, check_rows=16):
     return shape, fmt, mats, inp, specs, ws
 
 
-def run_sweep(name, steps, warmup, stream, wsr, want_cpu, cpu_seconds):
+def spread(ms, boot=2000, seed=0):
+    """Median, interquartile range and a 95 % bootstrap interval of the median over timed passes."""
+    a = np.asarray(ms, dtype=np.float64)
+    rng = np.random.default_rng(seed)
+    meds = np.median(a[rng.integers(0, len(a), size=(boot, len(a)))], axis=1)
+    return {"n": len(a), "ms_per_token": [round(float(v), 4) for v in a],
+            "median": round(float(np.median(a)), 4),
+            "iqr": [round(float(np.percentile(a, 25)), 4), round(float(np.percentile(a, 75)), 4)],
+            "ci95_median": [round(float(np.percentile(meds, 2.5)), 4), round(float(np.percentile(meds, 97.5)), 4)]}
+
+
+def run_sweep(name, steps, warmup, stream, wsr, want_cpu, cpu_seconds, passes=4):
     import torch
     from synth import workloads as wl
     shape, fmt, mats, inp, specs, ws = sweep_workload(name, max(steps, warmup, 1), stream, wsr)
@@ -126,6 +141,9 @@ def run_sweep(name, steps, warmup, stream, wsr, want_cpu, cpu_seconds):
     torch.cuda.synchronize()
     sec = timed(lambda: wsr.wsr_decode_sweep(specs, steps, ws, ws.numel(), stream), 1, stream)
     per_tok = sec / steps
+    # further timed passes of the same length, for the spread (the first pass above is the result)
+    pass_ms = [per_tok * 1e3] + [timed(lambda: wsr.wsr_decode_sweep(specs, steps, ws, ws.numel(), stream), 1,
+                                       stream) / steps * 1e3 for _ in range(passes)]
     gbps = bpt / per_tok / 1e9
     log(f"{name}: {steps} tokens in {sec * 1e3:.2f} ms -> {per_tok * 1e3:.3f} ms/token, "
         f"{gbps:.1f} GB/s ({gbps * 1e9 / HBM_PEAK * 100:.1f}% of 8 TB/s), {1 / per_tok:.2f} tok/s")
@@ -134,7 +152,7 @@ def run_sweep(name, steps, warmup, stream, wsr, want_cpu, cpu_seconds):
     out = {"workload": name, "bytes_per_token": bpt, "footprint_bytes": wl.footprint_bytes(shape, fmt),
            "tokens_timed": steps, "warmup_tokens": warmup, "ms_per_token": per_tok * 1e3,
            "GBps": gbps, "hbm_frac": gbps * 1e9 / HBM_PEAK, "tokens_per_s": 1 / per_tok,
-           "launches_per_token": 1, "parity": parity}
+           "launches_per_token": 1, "parity": parity, "passes": spread(pass_ms)}
     if want_cpu:
         out["cpu_baseline"] = cpu_baseline(inp, bpt, cpu_seconds)
     del specs, ws, inp
@@ -343,6 +361,35 @@ def row_bus(stream):
 
 # --------------------------------------------------------------------------------------------------
 
+def across_processes(args):
+    """The headline measured in separate processes (each its own inputs, warm-up and passes)."""
+    import subprocess
+    meds, firsts = [], []
+    for k in range(args.processes):
+        cmd = [sys.executable, os.path.abspath(__file__), "--workload", args.workload, "--rows", "",
+               "--no-cpu-baseline", "--steps", str(args.steps), "--warmup", str(args.warmup),
+               "--passes", str(args.passes)]
+        log(f"process {k + 1}/{args.processes}: {' '.join(cmd[1:])}")
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            sys.stderr.write(r.stdout[-2000:] + r.stderr[-2000:])
+            raise SystemExit(r.returncode)
+        line = json.loads([l for l in r.stdout.splitlines() if l.startswith("{")][-1])
+        meds.append(line["passes"]["median"])
+        firsts.append(line["ms_per_step"])
+        log(f"process {k + 1}: median {line['passes']['median']:.4f} ms/token over {line['passes']['n']} passes")
+    st = spread(meds)
+    bpt = None
+    from synth import workloads as wl
+    shape, fmt = SWEEPS[args.workload]
+    bpt = wl.bytes_per_token(getattr(wl, shape), fmt)
+    print(json.dumps({"workload": args.workload, "processes": args.processes, "steps": args.steps,
+                      "passes_per_process": args.passes + 1, "process_medians_ms": meds,
+                      "first_pass_ms": firsts, "median_of_medians_ms": st["median"],
+                      "iqr_ms": st["iqr"], "ci95_ms": st["ci95_median"],
+                      "GBps_at_median": round(bpt / (st["median"] * 1e-3) / 1e9, 2)}), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -351,6 +398,8 @@ def main():
                                    "multi-GPU form here (a sharded run would split rows across GPUs); "
                                    "run with --gpus 1"}))
         sys.exit(2)
+    if args.processes > 1:
+        return across_processes(args)
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     from paper_2608_12114_amd import wsr
@@ -359,7 +408,7 @@ def main():
     t_start = time.time()
 
     head = run_sweep(args.workload, args.steps, args.warmup, stream, wsr, not args.no_cpu_baseline,
-                     args.cpu_seconds)
+                     args.cpu_seconds, args.passes)
     rows = {}
     for r in [r for r in args.rows.split(",") if r]:
         if r == "probe":
@@ -397,6 +446,7 @@ def main():
                      "kernel": f"k_sweep ({dtype})", "bytes_per_launch": head["bytes_per_token"]},
         "cpu_baseline": head.get("cpu_baseline"),
         "parity": head["parity"],
+        "passes": head["passes"],
         "rows": rows,
         "wall_s": round(time.time() - t_start, 1),
     }
