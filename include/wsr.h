@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define WSR_ABI_VERSION 1
+#define WSR_ABI_VERSION 2
 
 typedef enum {
     WSR_OK = 0,
@@ -123,6 +123,18 @@ wsr_status wsr_gemv_f16(const void* W, const void* x, float* y, int64_t M, int64
 wsr_status wsr_gemv_q4(const uint8_t* Wq, const uint16_t* scales, const uint16_t* x, float* y,
                        int64_t M, int64_t K, void* stream);
 
+/* ---- multi-column GEMV (Sec. 3.4 and 5.2: T activation columns share each weight read) ---------
+
+   wsr_gemv_f16_cols: for t < T and i < M, y_t[i] = sum_k W[i*K + k] * x_t[k], where
+   x_t = x + t * x_col_stride bytes and y_t = y + t * y_col_stride bytes.  W, x_t and y_t follow
+   wsr_gemv_f16's layout, formats and alignment; T is 1, 2, 4, 8 or 16; x_col_stride >= 0 and a
+   multiple of 16 (0: every column reads the same x); y_col_stride a multiple of 4 and, for T > 1,
+   at least 4 M so that the output columns do not overlap (else WSR_E_ARG).  Every y_t is
+   bitwise equal to wsr_gemv_f16(W, x_t, y_t, M, K, fmt). */
+wsr_status wsr_gemv_f16_cols(const void* W, const void* x, int64_t x_col_stride, float* y,
+                             int64_t y_col_stride, int64_t M, int64_t K, int32_t T, int fmt,
+                             void* stream);
+
 /* ---- decode weight sweep ----------------------------------------------------------------------
 
    For t in [0, n_tokens), for m in [0, n) in order: y_m(t) = W_m . x_m(t), where
@@ -151,6 +163,16 @@ typedef struct wsr_mat {
 size_t wsr_sweep_workspace_bytes(const wsr_mat* mats, int32_t n);
 wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, void* ws,
                             size_t ws_bytes, void* stream);
+
+/* wsr_decode_sweep_batched: the same outputs as wsr_decode_sweep, bit for bit, with the tokens
+   taken `batch` at a time (1, 2, 4, 8 or 16): one pass over the weights serves tokens
+   t .. t + batch - 1, whose activations must all be ready when the call is made, as for a batch of
+   independent sequences or the candidates of a speculative step (Sec. 3.4, 5.2).  The last
+   n_tokens % batch tokens go in passes of the largest power of two that fits.  With batch > 1
+   every matrix must be 16-bit (q4 matrices: WSR_E_UNSUPPORTED) and have y_tok_stride >= 4 M.
+   ws as for wsr_decode_sweep. */
+wsr_status wsr_decode_sweep_batched(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch,
+                                    void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

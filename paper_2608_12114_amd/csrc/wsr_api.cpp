@@ -199,6 +199,30 @@ wsr_status wsr_gemv_f16(const void* W, const void* x, float* y, int64_t M, int64
     return ok();
 }
 
+wsr_status wsr_gemv_f16_cols(const void* W, const void* x, int64_t x_col_stride, float* y,
+                             int64_t y_col_stride, int64_t M, int64_t K, int32_t T, int fmt, void* stream) {
+    if (fmt != WSR_F16 && fmt != WSR_BF16)
+        return fail(WSR_E_ARG, "gemv_f16_cols: format must be WSR_F16 or WSR_BF16");
+    if (T != 1 && T != 2 && T != 4 && T != 8 && T != 16)
+        return fail(WSR_E_ARG, "gemv_f16_cols: T=%d must be 1, 2, 4, 8 or 16", T);
+    wsr_status st = check_matrix(fmt, M, K, W, nullptr, x, y, "gemv_f16_cols");
+    if (st != WSR_OK) return st;
+    if (x_col_stride < 0 || x_col_stride % 16 || y_col_stride < 0 || y_col_stride % 4)
+        return fail(WSR_E_ALIGN, "gemv_f16_cols: column strides must be >= 0 and multiples of 16 (x) and 4 (y)");
+    if (T > 1 && y_col_stride < M * 4)
+        return fail(WSR_E_ARG, "gemv_f16_cols: output columns overlap (y_col_stride %lld < 4 M)",
+                    (long long)y_col_stride);
+    if (!mul_fits(x_col_stride, T) || !mul_fits(y_col_stride, T))
+        return fail(WSR_E_SIZE, "gemv_f16_cols: column strides overflow");
+    if (M == 0) return ok();
+    DevMat d = make_devmat(fmt, M, K, W, nullptr, x, y);
+    d.x_stride = x_col_stride;
+    d.y_stride = y_col_stride;
+    const hipError_t e = wsr::launch_gemv_cols(d, T, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "gemv_f16_cols: launch");
+    return ok();
+}
+
 wsr_status wsr_gemv_q4(const uint8_t* Wq, const uint16_t* scales, const uint16_t* x, float* y,
                        int64_t M, int64_t K, void* stream) {
     wsr_status st = check_matrix(WSR_Q4, M, K, Wq, scales, x, y, "gemv_q4");
@@ -218,9 +242,15 @@ size_t wsr_sweep_workspace_bytes(const wsr_mat* mats, int32_t n) {
            ((size_t)n * sizeof(int64_t) + 255) / 256 * 256;
 }
 
-wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, void* ws,
-                            size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+wsr_status sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch, void* ws,
+                 size_t ws_bytes, void* stream) {
     if (n < 0 || n_tokens < 1) return fail(WSR_E_ARG, "decode_sweep: n=%d n_tokens=%d", n, n_tokens);
+    if (batch != 1 && batch != 2 && batch != 4 && batch != 8 && batch != 16)
+        return fail(WSR_E_ARG, "decode_sweep: batch=%d must be 1, 2, 4, 8 or 16", batch);
     if (n == 0) return ok();
     if (!mats || !ws) return fail(WSR_E_ARG, "decode_sweep: null pointer");
     if (!aligned(ws, 256)) return fail(WSR_E_ALIGN, "decode_sweep: workspace must be 256-byte aligned");
@@ -241,6 +271,10 @@ wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, vo
             return fail(WSR_E_ALIGN, "%s: token strides must be >= 0 and multiples of 16 (x) and 4 (y)", who);
         if (!mul_fits(m.x_tok_stride, n_tokens) || !mul_fits(m.y_tok_stride, n_tokens))
             return fail(WSR_E_SIZE, "%s: token strides overflow", who);
+        if (batch > 1 && m.fmt == WSR_Q4)
+            return fail(WSR_E_UNSUPPORTED, "%s: q4 matrices are swept one token per pass (batch 1)", who);
+        if (batch > 1 && m.M > 0 && m.y_tok_stride < m.M * 4)
+            return fail(WSR_E_ARG, "%s: tokens of one pass would share outputs (y_tok_stride < 4 M)", who);
         if (segs.empty() || (m.flags & WSR_MAT_AFTER_PREVIOUS)) segs.push_back(Seg{i, 0, m.fmt, 0});
         Seg& g = segs.back();
         DevMat d = make_devmat(m.fmt, m.M, m.K, m.w, m.scales, m.x, m.y);
@@ -261,12 +295,31 @@ wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, vo
                                                 ((size_t)n * sizeof(DevMat) + 255) / 256 * 256);
     hipError_t e = wsr::launch_put_table(dtab, dcost, tab.data(), n, ctr, s);
     if (e != hipSuccess) return hip_fail(e, "decode_sweep: table upload");
-    for (int32_t t = 0; t < n_tokens; ++t)
+    /* Passes of `batch` tokens; the last tokens go in passes of the largest power of two that fits. */
+    for (int32_t t = 0; t < n_tokens;) {
+        int32_t T = batch;
+        while (T > n_tokens - t) T >>= 1;
         for (const Seg& g : segs) {
-            e = wsr::launch_sweep(dtab + g.first, dcost + g.first, g.count, g.total, g.fmt, t, ctr, s);
+            e = wsr::launch_sweep(dtab + g.first, dcost + g.first, g.count, g.total, g.fmt, t, T, ctr, s);
             if (e != hipSuccess) return hip_fail(e, "decode_sweep: launch");
         }
+        t += T;
+    }
     return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, void* ws,
+                            size_t ws_bytes, void* stream) {
+    return sweep(mats, n, n_tokens, 1, ws, ws_bytes, stream);
+}
+
+wsr_status wsr_decode_sweep_batched(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch,
+                                    void* ws, size_t ws_bytes, void* stream) {
+    return sweep(mats, n, n_tokens, batch, ws, ws_bytes, stream);
 }
 
 }  // extern "C"

@@ -96,14 +96,19 @@ __device__ __forceinline__ double dpp_f64(double v) {
 /* Lane exchanges of the row reductions, in the order they are applied: lanes 32 apart, 16 apart,
    mirrored inside each 16-lane row (i <-> 15 - i), then the two quad swaps and the mirror inside
    each 8-lane half.  Each step pairs every lane with one partner, and together they join all 64. */
+/* The six exchanges of a wave reduction, in the order every reduction here uses.  Level k pairs
+   lane l with a partner that differs from l in lane bit 5 - k, and before level k every lane
+   differing from l only in lower bits holds the same set of partial sums, so the extra low bits
+   flipped by the mirrors do not matter: level 0 l ^ 32, level 1 l ^ 16, level 2 the row mirror
+   (l ^ 15), level 3 the half-row mirror (l ^ 7), level 4 l ^ 2, level 5 l ^ 1. */
 template <int LEVEL>
 __device__ __forceinline__ float xchg(float v) {
     if constexpr (LEVEL == 0) return __shfl_xor(v, 32);
     else if constexpr (LEVEL == 1) return __shfl_xor(v, 16);
     else if constexpr (LEVEL == 2) return dpp_f32<DPP_MIRROR>(v);
-    else if constexpr (LEVEL == 3) return dpp_f32<DPP_XOR1>(v);
+    else if constexpr (LEVEL == 3) return dpp_f32<DPP_HALF_MIRROR>(v);
     else if constexpr (LEVEL == 4) return dpp_f32<DPP_XOR2>(v);
-    else return dpp_f32<DPP_HALF_MIRROR>(v);
+    else return dpp_f32<DPP_XOR1>(v);
 }
 
 /* One transposed step: lanes whose `bit` is set keep the upper half of the row list and send the
@@ -121,25 +126,34 @@ __device__ __forceinline__ void halve_rows(float (&a)[N], int n, bool upper) {
     }
 }
 
-/* Totals of R per-lane partial sums (R = 1, 2, 4 or 8 rows) over the 64 lanes.  The first log2(R)
-   exchanges split the rows between partner lanes instead of duplicating them, so a group of R rows
-   costs about as much as one row; afterwards lane l holds the total of row l / (64 / R).  Every
-   row is summed by the same tree of pairwise additions whatever R is (each step adds a lane's
-   partial to its partner's, and a + b == b + a), so results do not depend on how rows were
-   grouped. */
-template <int R>
-__device__ __forceinline__ float wave_sum_rows(float (&a)[R], int lane) {
-    static_assert(R == 1 || R == 2 || R == 4 || R == 8, "R must be 1, 2, 4 or 8");
-    if constexpr (R >= 2) halve_rows<0, R>(a, R, lane & 32);
-    if constexpr (R >= 4) halve_rows<1, R>(a, R / 2, lane & 16);
-    if constexpr (R >= 8) halve_rows<2, R>(a, R / 4, lane & 8);
+/* Totals over the 64 lanes of N per-lane partial sums (N = 1, 2, 4, ..., 64: rows, or rows times
+   activation columns).  The first log2(N) exchanges split the list between partner lanes instead
+   of duplicating it, so N sums cost about as much as one; afterwards lane l holds the total of
+   entry l / (64 / N).  Every entry is summed by the same tree of pairwise additions whatever N is
+   (each level adds a lane's partial to its partner's, and a + b == b + a), so a result does not
+   depend on how rows or columns were grouped. */
+template <int LEVEL, int N>
+__device__ __forceinline__ void halve_level(float (&a)[N], int lane) {
+    constexpr int n = N >> LEVEL;                 /* entries still held before this level */
+    if constexpr (n >= 2) halve_rows<LEVEL, N>(a, n, lane & (32 >> LEVEL));
+}
+
+template <int N>
+__device__ __forceinline__ float wave_sum_rows(float (&a)[N], int lane) {
+    static_assert(N >= 1 && N <= 64 && (N & (N - 1)) == 0, "N must be a power of two up to 64");
+    halve_level<0, N>(a, lane);
+    halve_level<1, N>(a, lane);
+    halve_level<2, N>(a, lane);
+    halve_level<3, N>(a, lane);
+    halve_level<4, N>(a, lane);
+    halve_level<5, N>(a, lane);
     float v = a[0];
-    if constexpr (R < 2) v += xchg<0>(v);
-    if constexpr (R < 4) v += xchg<1>(v);
-    if constexpr (R < 8) v += xchg<2>(v);
-    v += xchg<3>(v);
-    v += xchg<4>(v);
-    v += xchg<5>(v);
+    if constexpr (N < 2) v += xchg<0>(v);
+    if constexpr (N < 4) v += xchg<1>(v);
+    if constexpr (N < 8) v += xchg<2>(v);
+    if constexpr (N < 16) v += xchg<3>(v);
+    if constexpr (N < 32) v += xchg<4>(v);
+    if constexpr (N < 64) v += xchg<5>(v);
     return v;
 }
 
@@ -206,6 +220,86 @@ __device__ __forceinline__ void group16(const char* W, g_u32x4* x, g_f32* y, int
     }
     const float s = wave_sum_rows<R>(acc, lane);
     if ((lane & (WAVE / R - 1)) == 0) y[i + lane / (WAVE / R)] = s;
+}
+
+/* Rows [i, i + R) against T activation columns read with one pass over the weights.  Column t of
+   the activations starts xcs 16-byte chunks after column 0 and its outputs ycs floats after
+   column 0's.  Each lane accumulates every (row, column) pair over the same chunk sequence as
+   group16, and the R * T sums go through the same reduction tree, so every column's result equals
+   the single-column result bit for bit. */
+template <int FMT, int R, int U, int T>
+__device__ __forceinline__ void group16_cols(const char* W, g_u32x4* x, int64_t xcs, g_f32* y, int64_t ycs,
+                                             int64_t nc, int64_t i, int lane) {
+    constexpr int STEP = WAVE * U;
+    constexpr int N = R * T;
+    float acc[N];                                   /* entry t * R + r */
+    g_u32x4* wr[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) wr[r] = as_global<g_u32x4*>(W + (i + r) * nc * 16);
+#pragma unroll
+    for (int e = 0; e < N; ++e) acc[e] = 0.f;
+    int64_t c0 = 0;
+    for (; c0 + STEP <= nc; c0 += STEP) {
+        u32x4 xv[T][U], wv[R][U];
+#pragma unroll
+        for (int t = 0; t < T; ++t)
+#pragma unroll
+            for (int u = 0; u < U; ++u) xv[t][u] = load_reused(x + t * xcs + c0 + u * WAVE + lane);
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+            for (int u = 0; u < U; ++u) wv[r][u] = load_once(wr[r] + c0 + u * WAVE + lane);
+#pragma unroll
+        for (int t = 0; t < T; ++t)
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int u = 0; u < U; ++u) acc[t * R + r] = dot8<FMT>(wv[r][u], xv[t][u], acc[t * R + r]);
+    }
+    if (c0 < nc) {  /* ragged last step */
+        u32x4 xv[T][U], wv[R][U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t c = c0 + u * WAVE + lane;
+#pragma unroll
+            for (int t = 0; t < T; ++t) xv[t][u] = c < nc ? load_reused(x + t * xcs + c) : zero4();
+#pragma unroll
+            for (int r = 0; r < R; ++r) wv[r][u] = c < nc ? load_once(wr[r] + c) : zero4();
+        }
+#pragma unroll
+        for (int t = 0; t < T; ++t)
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int u = 0; u < U; ++u) acc[t * R + r] = dot8<FMT>(wv[r][u], xv[t][u], acc[t * R + r]);
+    }
+    const float s = wave_sum_rows<N>(acc, lane);
+    if ((lane & (WAVE / N - 1)) == 0) {
+        const int e = lane / (WAVE / N);
+        y[(e / R) * ycs + i + e % R] = s;
+    }
+}
+
+/* Launch shape of the multi-column 16-bit row loops: rows per wave and chunks per lane per step for
+   T columns (about 8 KiB of weights per step and at most ~100 registers of operands). */
+template <int T> struct Cols16 { static constexpr int R = 1, U = 8; };
+template <> struct Cols16<2> { static constexpr int R = 2, U = 4; };
+template <> struct Cols16<4> { static constexpr int R = 2, U = 4; };
+template <> struct Cols16<8> { static constexpr int R = 4, U = 2; };
+template <> struct Cols16<16> { static constexpr int R = 4, U = 1; };
+
+/* Rows [r0, r1) of matrix d for tokens token0 .. token0 + T - 1 in one pass over the weights. */
+template <int FMT, int T>
+__device__ __forceinline__ void rows16_cols(const DevMat& d, int64_t r0, int64_t r1, int32_t token0,
+                                            int lane) {
+    constexpr int R = Cols16<T>::R, U = Cols16<T>::U;
+    const char* W = static_cast<const char*>(d.w);
+    g_u32x4* x = as_global<g_u32x4*>(static_cast<const char*>(d.x) + token0 * d.x_stride);
+    g_f32* y = as_global<g_f32*>(reinterpret_cast<char*>(d.y) + token0 * d.y_stride);
+    const int64_t xcs = d.x_stride / 16, ycs = d.y_stride / 4;
+    int64_t i = r0;
+    for (; i + R <= r1; i += R) group16_cols<FMT, R, U, T>(W, x, xcs, y, ycs, d.nc, i, lane);
+    for (; i < r1; ++i) group16_cols<FMT, 1, U, T>(W, x, xcs, y, ycs, d.nc, i, lane);
 }
 
 /* Rows [r0, r1) of matrix d at token `token` (r0, r1 wave-uniform): groups of R rows, then the
@@ -447,7 +541,7 @@ __device__ __forceinline__ void rows_q4(const DevMat& d, int64_t r0, int64_t r1,
 
 __device__ __forceinline__ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-template <int FMT, int R16, int U16, int RQ, int UQ, int QNB = 2>
+template <int FMT, int R16, int U16, int RQ, int UQ, int QNB = 2, int T = 1>
 __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, const int64_t* __restrict__ cost,
                                              int nmat, int64_t lo, int64_t hi, int32_t token, int lane,
                                              int& hint) {
@@ -470,17 +564,24 @@ __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, con
         /* A byte boundary maps to the first row group starting at or after it, the same way for
            the ranges on both sides, so the ranges still cover each row once and break only
            between whole groups of R rows. */
-        const int64_t g = fmt == FMT_Q4 ? RQ : R16;
+        const int64_t g = fmt == FMT_Q4 ? RQ : (T == 1 ? R16 : Cols16<T>::R);
         const int64_t r0 = lo > d.cost0 ? ceil_div(lo - d.cost0, d.row_bytes * g) * g : 0;
         const int64_t e1 = ceil_div(hi - d.cost0, d.row_bytes * g) * g;
         const int64_t r1 = d.M < e1 ? d.M : e1;
         if (r0 >= r1) continue;
-        if ((FMT == 0 || FMT == FMT_F16) && fmt == FMT_F16)
-            rows16<FMT_F16, R16, U16>(d, r0, r1, token, lane);
-        else if ((FMT == 0 || FMT == FMT_BF16) && fmt == FMT_BF16)
-            rows16<FMT_BF16, R16, U16>(d, r0, r1, token, lane);
-        else if ((FMT == 0 || FMT == FMT_Q4) && fmt == FMT_Q4)
-            rows_q4<RQ, UQ, QNB>(d, r0, r1, token, lane);
+        if constexpr (T == 1) {
+            if ((FMT == 0 || FMT == FMT_F16) && fmt == FMT_F16)
+                rows16<FMT_F16, R16, U16>(d, r0, r1, token, lane);
+            else if ((FMT == 0 || FMT == FMT_BF16) && fmt == FMT_BF16)
+                rows16<FMT_BF16, R16, U16>(d, r0, r1, token, lane);
+            else if ((FMT == 0 || FMT == FMT_Q4) && fmt == FMT_Q4)
+                rows_q4<RQ, UQ, QNB>(d, r0, r1, token, lane);
+        } else {                                        /* tokens token .. token + T - 1 together */
+            if ((FMT == 0 || FMT == FMT_F16) && fmt == FMT_F16)
+                rows16_cols<FMT_F16, T>(d, r0, r1, token, lane);
+            else if ((FMT == 0 || FMT == FMT_BF16) && fmt == FMT_BF16)
+                rows16_cols<FMT_BF16, T>(d, r0, r1, token, lane);
+        }
     }
 }
 

@@ -144,6 +144,36 @@ static hipError_t launch_rows(K kernel, const DevMat& m, int R, hipStream_t s) {
     return hipGetLastError();
 }
 
+/* T activation columns per weight read (x_stride / y_stride of d are the column strides). */
+template <int FMT, int T>
+__global__ __launch_bounds__(BLOCK) void k_gemv16_cols(DevMat d) {
+    constexpr int R = Cols16<T>::R;
+    const int lane = threadIdx.x & (WAVE - 1);
+    const int64_t wave = (int64_t)blockIdx.x * WAVES_PER_BLOCK + wave_in_block();
+    const int64_t r0 = wave * R;
+    if (r0 >= d.M) return;
+    rows16_cols<FMT, T>(d, r0, std::min<int64_t>(r0 + R, d.M), 0, lane);
+}
+
+template <int FMT>
+static hipError_t launch_gemv16_cols(const DevMat& m, int T, hipStream_t s) {
+    switch (T) {
+        case 1: return launch_rows(k_gemv16_cols<FMT, 1>, m, Cols16<1>::R, s);
+        case 2: return launch_rows(k_gemv16_cols<FMT, 2>, m, Cols16<2>::R, s);
+        case 4: return launch_rows(k_gemv16_cols<FMT, 4>, m, Cols16<4>::R, s);
+        case 8: return launch_rows(k_gemv16_cols<FMT, 8>, m, Cols16<8>::R, s);
+        case 16: return launch_rows(k_gemv16_cols<FMT, 16>, m, Cols16<16>::R, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_gemv_cols(const DevMat& m, int T, hipStream_t s) {
+    if (m.M == 0) return hipSuccess;
+    if (m.fmt == FMT_F16) return launch_gemv16_cols<FMT_F16>(m, T, s);
+    if (m.fmt == FMT_BF16) return launch_gemv16_cols<FMT_BF16>(m, T, s);
+    return hipErrorInvalidValue;
+}
+
 hipError_t launch_gemv(const DevMat& m, hipStream_t s) {
     if (m.M == 0) return hipSuccess;
     switch (m.fmt) {
@@ -211,7 +241,7 @@ int64_t sweep_tile(int64_t total, int64_t waves) {
                    waves that finish early share the remainder.
    The counters ctr[0] (next tile) and ctr[1] (waves done) start at zero and the last wave to
    finish puts them back to zero for the next launch. */
-template <int FMT, int SCHED, int R16, int U16, int RQ, int UQ, int QNB = 2>
+template <int FMT, int SCHED, int R16, int U16, int RQ, int UQ, int QNB = 2, int T = 1>
 __global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab, const int64_t* __restrict__ cost,
                                                  int nmat, int64_t total, int64_t span, int64_t tile,
                                                  int32_t token, unsigned* __restrict__ ctr) {
@@ -224,12 +254,12 @@ __global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab,
         const int64_t q = total / nw, r = total % nw;
         const int64_t lo = q * w + (int64_t)((uint64_t)r * (uint64_t)w / nw);
         const int64_t hi = q * (w + 1) + (int64_t)((uint64_t)r * (uint64_t)(w + 1) / nw);
-        if (lo < hi) stream_range<FMT, R16, U16, RQ, UQ, QNB>(tab, cost, nmat, lo, hi, token, lane, hint);
+        if (lo < hi) stream_range<FMT, R16, U16, RQ, UQ, QNB, T>(tab, cost, nmat, lo, hi, token, lane, hint);
     } else {
         int64_t base = 0;
         if constexpr (SCHED == SCHED_HYBRID) {
             base = span * nw;
-            if (span > 0) stream_range<FMT, R16, U16, RQ, UQ, QNB>(tab, cost, nmat, span * w, span * (w + 1),
+            if (span > 0) stream_range<FMT, R16, U16, RQ, UQ, QNB, T>(tab, cost, nmat, span * w, span * (w + 1),
                                                                    token, lane, hint);
         }
         /* Each wave claims its next tile before working on the current one, so the round trip of
@@ -242,7 +272,7 @@ __global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab,
             if ((int64_t)t >= ntiles) break;
             if (lane == 0) claim = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             const int64_t lo = base + (int64_t)t * tile;
-            stream_range<FMT, R16, U16, RQ, UQ, QNB>(tab, cost, nmat, lo, std::min<int64_t>(total, lo + tile),
+            stream_range<FMT, R16, U16, RQ, UQ, QNB, T>(tab, cost, nmat, lo, std::min<int64_t>(total, lo + tile),
                                                      token, lane, hint);
         }
         if (lane == 0) {
@@ -275,34 +305,50 @@ static int cu_count() {
 constexpr int SWEEP_BLOCKS_PER_CU_16 = 1;
 constexpr int64_t SWEEP_SPAN_Q4 = 64 << 10;
 
+/* 16-bit (or mixed-format) sweep over tiles, tokens token .. token + T - 1 per weight pass. */
+template <int FMT, int T>
+static void launch_sweep_tiles(dim3 grid, hipStream_t s, const DevMat* tab, const int64_t* cost, int nmat,
+                               int64_t total, int64_t tile, int32_t token, unsigned* ctr) {
+    hipLaunchKernelGGL((k_sweep<FMT, SCHED_TILES, 4, 4, 8, 1, 2, T>), grid, dim3(BLOCK), 0, s, tab, cost, nmat,
+                       total, (int64_t)0, tile, token, ctr);
+}
+
+template <int FMT>
+static hipError_t launch_sweep_cols(dim3 grid, int T, hipStream_t s, const DevMat* tab, const int64_t* cost,
+                                    int nmat, int64_t total, int64_t tile, int32_t token, unsigned* ctr) {
+    switch (T) {
+        case 1: launch_sweep_tiles<FMT, 1>(grid, s, tab, cost, nmat, total, tile, token, ctr); break;
+        case 2: launch_sweep_tiles<FMT, 2>(grid, s, tab, cost, nmat, total, tile, token, ctr); break;
+        case 4: launch_sweep_tiles<FMT, 4>(grid, s, tab, cost, nmat, total, tile, token, ctr); break;
+        case 8: launch_sweep_tiles<FMT, 8>(grid, s, tab, cost, nmat, total, tile, token, ctr); break;
+        case 16: launch_sweep_tiles<FMT, 16>(grid, s, tab, cost, nmat, total, tile, token, ctr); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, int nmat, int64_t total, int fmt_all,
-                        int32_t token, unsigned* ctr, hipStream_t s) {
+                        int32_t token, int T, unsigned* ctr, hipStream_t s) {
     if (nmat == 0 || total == 0) return hipSuccess;
-    const dim3 block(BLOCK);
     if (fmt_all == FMT_Q4) {
+        if (T != 1) return hipErrorInvalidValue;
         /* About SWEEP_SPAN_Q4 bytes per wave, at least one wave per SIMD. */
         const int64_t waves = std::max<int64_t>((int64_t)cu_count() * WAVES_PER_BLOCK,
                                                 (total + SWEEP_SPAN_Q4 - 1) / SWEEP_SPAN_Q4);
         const int64_t blocks = (waves + WAVES_PER_BLOCK - 1) / WAVES_PER_BLOCK;
         if (blocks > INT32_MAX) return hipErrorInvalidValue;
-        hipLaunchKernelGGL((k_sweep<FMT_Q4, SCHED_SPANS, 4, 4, 8, 1>), dim3((unsigned)blocks), block, 0, s, tab, cost,
-                           nmat, total, (int64_t)0, (int64_t)0, token, ctr);
+        hipLaunchKernelGGL((k_sweep<FMT_Q4, SCHED_SPANS, 4, 4, 8, 1>), dim3((unsigned)blocks), dim3(BLOCK), 0, s,
+                           tab, cost, nmat, total, (int64_t)0, (int64_t)0, token, ctr);
         return hipGetLastError();
     }
     const dim3 grid((unsigned)(cu_count() * SWEEP_BLOCKS_PER_CU_16));
     const int64_t tile = sweep_tile(total, (int64_t)grid.x * WAVES_PER_BLOCK);
     switch (fmt_all) {
-        case FMT_F16:
-            hipLaunchKernelGGL((k_sweep<FMT_F16, SCHED_TILES, 4, 4, 8, 1>), grid, block, 0, s, tab, cost, nmat, total, (int64_t)0, tile, token, ctr);
-            break;
-        case FMT_BF16:
-            hipLaunchKernelGGL((k_sweep<FMT_BF16, SCHED_TILES, 4, 4, 8, 1>), grid, block, 0, s, tab, cost, nmat, total, (int64_t)0, tile, token, ctr);
-            break;
-        default:
-            hipLaunchKernelGGL((k_sweep<0, SCHED_TILES, 4, 4, 8, 1>), grid, block, 0, s, tab, cost, nmat, total, (int64_t)0, tile, token, ctr);
-            break;
+        case FMT_F16: return launch_sweep_cols<FMT_F16>(grid, T, s, tab, cost, nmat, total, tile, token, ctr);
+        case FMT_BF16: return launch_sweep_cols<FMT_BF16>(grid, T, s, tab, cost, nmat, total, tile, token, ctr);
+        default:   /* mixed formats; with T > 1 the caller has checked that none is q4 */
+            return launch_sweep_cols<0>(grid, T, s, tab, cost, nmat, total, tile, token, ctr);
     }
-    return hipGetLastError();
 }
 
 }  // namespace wsr

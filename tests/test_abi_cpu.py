@@ -21,13 +21,13 @@ def declared():
 
 def test_exports_every_declared_symbol():
     names = declared()
-    assert len(names) == 10, names
+    assert len(names) == 12, names
     for n in names:
         assert hasattr(L, n), n
 
 
 def test_version_and_status_values():
-    assert wsr.wsr_abi_version() == 1
+    assert wsr.wsr_abi_version() == 2
     m = re.search(r"#define WSR_ABI_VERSION (\d+)", HEADER)
     assert int(m.group(1)) == wsr.wsr_abi_version()
     for name, val in (("WSR_OK", 0), ("WSR_E_ARG", 1), ("WSR_E_ALIGN", 2), ("WSR_E_SIZE", 3),
@@ -73,6 +73,37 @@ def test_probe_argument_checks():
     assert _status(f, A + 4, 8, A, A, need, None) == wsr.WSR_E_ALIGN
     assert _status(f, A, 8, A + 4, A, need, None) == wsr.WSR_E_ALIGN
     assert _status(f, A, 1 << 28, A, A, need - 8, None) == wsr.WSR_E_SIZE
+
+
+def test_gemv_cols_argument_checks():
+    f = "wsr_gemv_f16_cols"
+    # (W, x, x_col_stride, y, y_col_stride, M, K, T, fmt, stream)
+    assert _status(f, A, A, 16, A, 64, 4, 8, 2, 9, None) == wsr.WSR_E_ARG        # unknown format
+    assert _status(f, A, A, 16, A, 64, 4, 8, 2, wsr.WSR_Q4, None) == wsr.WSR_E_ARG
+    for T in (0, 3, 5, 32, -1):
+        assert _status(f, A, A, 16, A, 64, 4, 8, T, 1, None) == wsr.WSR_E_ARG, T  # T not a power of two <= 16
+    assert _status(f, A, A, 8, A, 64, 4, 8, 2, 1, None) == wsr.WSR_E_ALIGN         # x stride % 16
+    assert _status(f, A, A, -16, A, 64, 4, 8, 2, 1, None) == wsr.WSR_E_ALIGN
+    assert _status(f, A, A, 16, A, 6, 4, 8, 2, 1, None) == wsr.WSR_E_ALIGN         # y stride % 4
+    assert _status(f, A, A, 16, A, 12, 4, 8, 2, 1, None) == wsr.WSR_E_ARG          # output columns overlap
+    assert _status(f, A, A, 16, A, 16, 4, 12, 2, 1, None) == wsr.WSR_E_ALIGN       # K % 8
+    assert _status(f, None, None, 0, None, 0, 0, 8, 4, 1, None) == wsr.WSR_OK      # M = 0
+
+
+def test_batched_sweep_argument_checks():
+    good = dict(fmt=2, M=8, K=64, w=A, x=A, y=A, x_tok_stride=128, y_tok_stride=32)
+    mats = wsr.make_mats([good, good])
+    ws = wsr.wsr_sweep_workspace_bytes(mats)
+    f = "wsr_decode_sweep_batched"
+    for b in (0, 3, 32, -2):
+        assert _status(f, mats, 2, 4, b, A, ws, None) == wsr.WSR_E_ARG, b
+    q = wsr.make_mats([good, dict(good, fmt=3, scales=A)])
+    assert _status(f, q, 2, 4, 2, A, ws, None) == wsr.WSR_E_UNSUPPORTED            # q4 takes batch 1
+    assert "batch 1" in wsr.wsr_last_error()
+    shared = wsr.make_mats([good, dict(good, y_tok_stride=0)])
+    assert _status(f, shared, 2, 4, 2, A, ws, None) == wsr.WSR_E_ARG               # tokens would share y
+    assert _status(f, mats, 2, 0, 2, A, ws, None) == wsr.WSR_E_ARG                 # n_tokens < 1
+    assert _status(f, mats, 2, 4, 2, A, ws - 1, None) == wsr.WSR_E_SIZE
 
 
 def test_sweep_argument_checks():
