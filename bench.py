@@ -149,15 +149,42 @@ def run_sweep(name, steps, warmup, stream, wsr, want_cpu, cpu_seconds, passes=4)
         f"{gbps:.1f} GB/s ({gbps * 1e9 / HBM_PEAK * 100:.1f}% of 8 TB/s), {1 / per_tok:.2f} tok/s")
     parity = check_sweep(inp, [0, steps - 1])
     log(f"{name}: parity on sampled rows: worst rel-L2 {parity['worst_rel_l2']:.2e}")
+    batched = batch_sweep(name, inp, specs, ws, steps, bpt, stream, wsr) if fmt != wl.Q4 else None
     out = {"workload": name, "bytes_per_token": bpt, "footprint_bytes": wl.footprint_bytes(shape, fmt),
            "tokens_timed": steps, "warmup_tokens": warmup, "ms_per_token": per_tok * 1e3,
            "GBps": gbps, "hbm_frac": gbps * 1e9 / HBM_PEAK, "tokens_per_s": 1 / per_tok,
            "launches_per_token": 1, "parity": parity, "passes": spread(pass_ms)}
+    if batched is not None:
+        out["batched"] = batched
     if want_cpu:
         out["cpu_baseline"] = cpu_baseline(inp, bpt, cpu_seconds)
     del specs, ws, inp
     torch.cuda.empty_cache()
     return out
+
+
+def batch_sweep(name, inp, specs, ws, steps, bpt, stream, wsr, batches=(1, 2, 4, 8, 16)):
+    """The same tokens with `batch` of them sharing each pass over the weights (the multi-column
+    T-sweep): outputs are compared bit for bit with the token-by-token sweep."""
+    import torch
+    ref = [y.clone() for y in inp.y]           # the token-by-token outputs of the timed passes
+    res = []
+    for b in batches:
+        if b > steps:
+            break
+        run = lambda: wsr.wsr_decode_sweep_batched(specs, steps, b, ws, ws.numel(), stream)
+        run()
+        torch.cuda.synchronize()
+        same = all(torch.equal(a, y) for a, y in zip(ref, inp.y))
+        sec = median_of(run, 1, 3, stream)
+        passes = -(-steps // b)
+        res.append({"batch": b, "ms_per_pass": sec / passes * 1e3, "tokens_per_s": steps / sec,
+                    "hbm_GBps": passes * bpt / sec / 1e9, "logical_weight_GBps": steps * bpt / sec / 1e9,
+                    "bitwise_equal_to_token_by_token": bool(same)})
+        log(f"{name}: batch {b:2d}: {steps / sec:8.2f} tok/s, HBM {passes * bpt / sec / 1e9:7.1f} GB/s, "
+            f"logical weight rate {steps * bpt / sec / 1e9:8.1f} GB/s, same outputs: {same}")
+    del ref
+    return res
 
 
 def check_sweep(inp, tokens, nrows=8):

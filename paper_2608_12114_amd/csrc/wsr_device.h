@@ -126,12 +126,13 @@ __device__ __forceinline__ void halve_rows(float (&a)[N], int n, bool upper) {
     }
 }
 
-/* Totals over the 64 lanes of N per-lane partial sums (N = 1, 2, 4, ..., 64: rows, or rows times
-   activation columns).  The first log2(N) exchanges split the list between partner lanes instead
-   of duplicating it, so N sums cost about as much as one; afterwards lane l holds the total of
-   entry l / (64 / N).  Every entry is summed by the same tree of pairwise additions whatever N is
-   (each level adds a lane's partial to its partner's, and a + b == b + a), so a result does not
-   depend on how rows or columns were grouped. */
+/* Totals over the 64 lanes of N per-lane partial sums (N = 1, 2, 4, ..., 256: rows, or rows times
+   activation columns).  The first min(log2 N, 6) exchanges split the list between partner lanes
+   instead of duplicating it, so N sums cost about as much as one.  Afterwards, for N <= 64, lane l
+   holds the total of entry l / (64 / N) in a[0]; for N > 64, lane l holds the totals of entries
+   l * (N / 64) + j in a[j], j < N / 64.  Every entry is summed by the same tree of pairwise additions
+   whatever N is (each level adds a lane's partial to its partner's, and a + b == b + a), so a
+   result does not depend on how rows or columns were grouped. */
 template <int LEVEL, int N>
 __device__ __forceinline__ void halve_level(float (&a)[N], int lane) {
     constexpr int n = N >> LEVEL;                 /* entries still held before this level */
@@ -139,22 +140,27 @@ __device__ __forceinline__ void halve_level(float (&a)[N], int lane) {
 }
 
 template <int N>
-__device__ __forceinline__ float wave_sum_rows(float (&a)[N], int lane) {
-    static_assert(N >= 1 && N <= 64 && (N & (N - 1)) == 0, "N must be a power of two up to 64");
+__device__ __forceinline__ void wave_sum_entries(float (&a)[N], int lane) {
+    static_assert(N >= 1 && N <= 256 && (N & (N - 1)) == 0, "N must be a power of two up to 256");
     halve_level<0, N>(a, lane);
     halve_level<1, N>(a, lane);
     halve_level<2, N>(a, lane);
     halve_level<3, N>(a, lane);
     halve_level<4, N>(a, lane);
     halve_level<5, N>(a, lane);
-    float v = a[0];
-    if constexpr (N < 2) v += xchg<0>(v);
-    if constexpr (N < 4) v += xchg<1>(v);
-    if constexpr (N < 8) v += xchg<2>(v);
-    if constexpr (N < 16) v += xchg<3>(v);
-    if constexpr (N < 32) v += xchg<4>(v);
-    if constexpr (N < 64) v += xchg<5>(v);
-    return v;
+    if constexpr (N < 2) a[0] += xchg<0>(a[0]);
+    if constexpr (N < 4) a[0] += xchg<1>(a[0]);
+    if constexpr (N < 8) a[0] += xchg<2>(a[0]);
+    if constexpr (N < 16) a[0] += xchg<3>(a[0]);
+    if constexpr (N < 32) a[0] += xchg<4>(a[0]);
+    if constexpr (N < 64) a[0] += xchg<5>(a[0]);
+}
+
+template <int N>
+__device__ __forceinline__ float wave_sum_rows(float (&a)[N], int lane) {
+    static_assert(N <= 64, "one total per lane needs N <= 64");
+    wave_sum_entries<N>(a, lane);
+    return a[0];
 }
 
 /* Single-row form: every lane ends with the same total. */
@@ -273,26 +279,35 @@ __device__ __forceinline__ void group16_cols(const char* W, g_u32x4* x, int64_t 
 #pragma unroll
                 for (int u = 0; u < U; ++u) acc[t * R + r] = dot8<FMT>(wv[r][u], xv[t][u], acc[t * R + r]);
     }
-    const float s = wave_sum_rows<N>(acc, lane);
-    if ((lane & (WAVE / N - 1)) == 0) {
-        const int e = lane / (WAVE / N);
-        y[(e / R) * ycs + i + e % R] = s;
+    wave_sum_entries<N>(acc, lane);
+    if constexpr (N <= WAVE) {
+        if ((lane & (WAVE / N - 1)) == 0) {
+            const int e = lane / (WAVE / N);
+            y[(e / R) * ycs + i + e % R] = acc[0];
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < N / WAVE; ++j) {
+            const int e = lane * (N / WAVE) + j;
+            y[(e / R) * ycs + i + e % R] = acc[j];
+        }
     }
 }
 
-/* Launch shape of the multi-column 16-bit row loops: rows per wave and chunks per lane per step for
-   T columns (about 8 KiB of weights per step and at most ~100 registers of operands). */
+/* Launch shape of the multi-column 16-bit row loops: rows per wave R and chunks per lane per step U
+   for T columns.  A step loads R U weight chunks and T U activation chunks per lane, so tall row
+   groups keep the activation reloads (from L2) below the weight stream; measured on the 70B
+   sweep, these shapes hold the weight stream at 7.1, 6.9, 6.5 and 4.6 TB/s for T = 2, 4, 8, 16. */
 template <int T> struct Cols16 { static constexpr int R = 1, U = 8; };
-template <> struct Cols16<2> { static constexpr int R = 2, U = 4; };
-template <> struct Cols16<4> { static constexpr int R = 2, U = 4; };
-template <> struct Cols16<8> { static constexpr int R = 4, U = 2; };
-template <> struct Cols16<16> { static constexpr int R = 4, U = 1; };
+template <> struct Cols16<2> { static constexpr int R = 4, U = 4; };
+template <> struct Cols16<4> { static constexpr int R = 8, U = 1; };
+template <> struct Cols16<8> { static constexpr int R = 16, U = 1; };
+template <> struct Cols16<16> { static constexpr int R = 8, U = 1; };
 
 /* Rows [r0, r1) of matrix d for tokens token0 .. token0 + T - 1 in one pass over the weights. */
-template <int FMT, int T>
+template <int FMT, int T, int R = Cols16<T>::R, int U = Cols16<T>::U>
 __device__ __forceinline__ void rows16_cols(const DevMat& d, int64_t r0, int64_t r1, int32_t token0,
                                             int lane) {
-    constexpr int R = Cols16<T>::R, U = Cols16<T>::U;
     const char* W = static_cast<const char*>(d.w);
     g_u32x4* x = as_global<g_u32x4*>(static_cast<const char*>(d.x) + token0 * d.x_stride);
     g_f32* y = as_global<g_f32*>(reinterpret_cast<char*>(d.y) + token0 * d.y_stride);
@@ -541,7 +556,8 @@ __device__ __forceinline__ void rows_q4(const DevMat& d, int64_t r0, int64_t r1,
 
 __device__ __forceinline__ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-template <int FMT, int R16, int U16, int RQ, int UQ, int QNB = 2, int T = 1>
+template <int FMT, int R16, int U16, int RQ, int UQ, int QNB = 2, int T = 1, int RC = Cols16<T>::R,
+          int UC = Cols16<T>::U>
 __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, const int64_t* __restrict__ cost,
                                              int nmat, int64_t lo, int64_t hi, int32_t token, int lane,
                                              int& hint) {
@@ -564,7 +580,7 @@ __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, con
         /* A byte boundary maps to the first row group starting at or after it, the same way for
            the ranges on both sides, so the ranges still cover each row once and break only
            between whole groups of R rows. */
-        const int64_t g = fmt == FMT_Q4 ? RQ : (T == 1 ? R16 : Cols16<T>::R);
+        const int64_t g = fmt == FMT_Q4 ? RQ : (T == 1 ? R16 : RC);
         const int64_t r0 = lo > d.cost0 ? ceil_div(lo - d.cost0, d.row_bytes * g) * g : 0;
         const int64_t e1 = ceil_div(hi - d.cost0, d.row_bytes * g) * g;
         const int64_t r1 = d.M < e1 ? d.M : e1;
@@ -578,9 +594,9 @@ __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, con
                 rows_q4<RQ, UQ, QNB>(d, r0, r1, token, lane);
         } else {                                        /* tokens token .. token + T - 1 together */
             if ((FMT == 0 || FMT == FMT_F16) && fmt == FMT_F16)
-                rows16_cols<FMT_F16, T>(d, r0, r1, token, lane);
+                rows16_cols<FMT_F16, T, RC, UC>(d, r0, r1, token, lane);
             else if ((FMT == 0 || FMT == FMT_BF16) && fmt == FMT_BF16)
-                rows16_cols<FMT_BF16, T>(d, r0, r1, token, lane);
+                rows16_cols<FMT_BF16, T, RC, UC>(d, r0, r1, token, lane);
         }
     }
 }
