@@ -135,6 +135,13 @@ wsr_status wsr_gemv_f16_cols(const void* W, const void* x, int64_t x_col_stride,
                              int64_t y_col_stride, int64_t M, int64_t K, int32_t T, int fmt,
                              void* stream);
 
+/* wsr_gemv_q4_cols: the same for q4 weights (wsr_gemv_q4's layout), T = 1, 2, 4 or 8: each
+   block is decoded once and used for every column.  Every y_t is bitwise equal to
+   wsr_gemv_q4(Wq, scales, x_t, y_t, M, K). */
+wsr_status wsr_gemv_q4_cols(const uint8_t* Wq, const uint16_t* scales, const uint16_t* x,
+                            int64_t x_col_stride, float* y, int64_t y_col_stride, int64_t M, int64_t K,
+                            int32_t T, void* stream);
+
 /* ---- decode weight sweep ----------------------------------------------------------------------
 
    For t in [0, n_tokens), for m in [0, n) in order: y_m(t) = W_m . x_m(t), where
@@ -168,9 +175,9 @@ wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, vo
    taken `batch` at a time (1, 2, 4, 8 or 16): one pass over the weights serves tokens
    t .. t + batch - 1, whose activations must all be ready when the call is made, as for a batch of
    independent sequences or the candidates of a speculative step (Sec. 3.4, 5.2).  The last
-   n_tokens % batch tokens go in passes of the largest power of two that fits.  With batch > 1
-   every matrix must be 16-bit (q4 matrices: WSR_E_UNSUPPORTED) and have y_tok_stride >= 4 M.
-   ws as for wsr_decode_sweep. */
+   n_tokens % batch tokens go in passes of the largest power of two that fits.  A table holding a
+   q4 matrix is swept at most 8 tokens per pass (batch 16 acts as 8).  With batch > 1 every matrix
+   must have y_tok_stride >= 4 M.  ws as for wsr_decode_sweep. */
 wsr_status wsr_decode_sweep_batched(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch,
                                     void* ws, size_t ws_bytes, void* stream);
 

@@ -223,6 +223,29 @@ wsr_status wsr_gemv_f16_cols(const void* W, const void* x, int64_t x_col_stride,
     return ok();
 }
 
+wsr_status wsr_gemv_q4_cols(const uint8_t* Wq, const uint16_t* scales, const uint16_t* x,
+                            int64_t x_col_stride, float* y, int64_t y_col_stride, int64_t M, int64_t K,
+                            int32_t T, void* stream) {
+    if (T != 1 && T != 2 && T != 4 && T != 8)
+        return fail(WSR_E_ARG, "gemv_q4_cols: T=%d must be 1, 2, 4 or 8", T);
+    wsr_status st = check_matrix(WSR_Q4, M, K, Wq, scales, x, y, "gemv_q4_cols");
+    if (st != WSR_OK) return st;
+    if (x_col_stride < 0 || x_col_stride % 16 || y_col_stride < 0 || y_col_stride % 4)
+        return fail(WSR_E_ALIGN, "gemv_q4_cols: column strides must be >= 0 and multiples of 16 (x) and 4 (y)");
+    if (T > 1 && y_col_stride < M * 4)
+        return fail(WSR_E_ARG, "gemv_q4_cols: output columns overlap (y_col_stride %lld < 4 M)",
+                    (long long)y_col_stride);
+    if (!mul_fits(x_col_stride, T) || !mul_fits(y_col_stride, T))
+        return fail(WSR_E_SIZE, "gemv_q4_cols: column strides overflow");
+    if (M == 0) return ok();
+    DevMat d = make_devmat(WSR_Q4, M, K, Wq, scales, x, y);
+    d.x_stride = x_col_stride;
+    d.y_stride = y_col_stride;
+    const hipError_t e = wsr::launch_gemv_cols(d, T, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "gemv_q4_cols: launch");
+    return ok();
+}
+
 wsr_status wsr_gemv_q4(const uint8_t* Wq, const uint16_t* scales, const uint16_t* x, float* y,
                        int64_t M, int64_t K, void* stream) {
     wsr_status st = check_matrix(WSR_Q4, M, K, Wq, scales, x, y, "gemv_q4");
@@ -271,8 +294,6 @@ wsr_status sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch
             return fail(WSR_E_ALIGN, "%s: token strides must be >= 0 and multiples of 16 (x) and 4 (y)", who);
         if (!mul_fits(m.x_tok_stride, n_tokens) || !mul_fits(m.y_tok_stride, n_tokens))
             return fail(WSR_E_SIZE, "%s: token strides overflow", who);
-        if (batch > 1 && m.fmt == WSR_Q4)
-            return fail(WSR_E_UNSUPPORTED, "%s: q4 matrices are swept one token per pass (batch 1)", who);
         if (batch > 1 && m.M > 0 && m.y_tok_stride < m.M * 4)
             return fail(WSR_E_ARG, "%s: tokens of one pass would share outputs (y_tok_stride < 4 M)", who);
         if (segs.empty() || (m.flags & WSR_MAT_AFTER_PREVIOUS)) segs.push_back(Seg{i, 0, m.fmt, 0});
@@ -295,7 +316,10 @@ wsr_status sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch
                                                 ((size_t)n * sizeof(DevMat) + 255) / 256 * 256);
     hipError_t e = wsr::launch_put_table(dtab, dcost, tab.data(), n, ctr, s);
     if (e != hipSuccess) return hip_fail(e, "decode_sweep: table upload");
-    /* Passes of `batch` tokens; the last tokens go in passes of the largest power of two that fits. */
+    /* Passes of `batch` tokens (at most 8 when the table holds q4 matrices); the last tokens go in
+       passes of the largest power of two that fits. */
+    for (int32_t i = 0; i < n && batch > 8; ++i)
+        if (mats[i].fmt == WSR_Q4) batch = 8;
     for (int32_t t = 0; t < n_tokens;) {
         int32_t T = batch;
         while (T > n_tokens - t) T >>= 1;

@@ -485,6 +485,107 @@ __device__ __forceinline__ void q4_group(g_u32x4* Wq, g_u16* S, g_u32x4* x, g_f3
     q4_store<R>(y, i, acc, lane);
 }
 
+/* Rows [i, i + R) of a q4 matrix against T activation columns in one pass over the codes: each
+   row's block is decoded once per step and dotted with every column's activation pairs.  Per
+   (row, column) the arithmetic and its order are those of q4_block_dot and q4_store, and the
+   R * T totals share the reduction tree, so each column equals the single-column result bit for
+   bit.  Column t of x starts xcs 16-byte chunks after column 0, its outputs ycs floats after. */
+template <int R, int T>
+__device__ __forceinline__ void q4_group_cols(g_u32x4* Wq, g_u16* S, g_u32x4* x, int64_t xcs, g_f32* y,
+                                              int64_t ycs, int64_t nb, int64_t i, int lane) {
+    constexpr int N = R * T;
+    float acc[N];                                   /* entry t * R + r */
+#pragma unroll
+    for (int e = 0; e < N; ++e) acc[e] = 0.f;
+    g_u32x4* wr[R];
+    g_u16* sr[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        wr[r] = Wq + (i + r) * nb;
+        sr[r] = S + (i + r) * nb;
+    }
+    for (int64_t b0 = 0; b0 < nb; b0 += WAVE) {
+        const int64_t b = b0 + lane;
+        const bool ok = b < nb;
+        u32x4 xv[T][4], wv[R];
+        uint16_t sv[R];
+#pragma unroll
+        for (int t = 0; t < T; ++t)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) xv[t][j] = ok ? load_reused(x + t * xcs + 4 * b + j) : zero4();
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            wv[r] = ok ? load_once(wr[r] + b) : zero4();
+            sv[r] = ok ? sr[r][b] : (uint16_t)0;
+        }
+        uint32_t dec[R][16];                        /* decoded subnormal pairs, q4_block_dot's order */
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const uint32_t wd[4] = {wv[r].x, wv[r].y, wv[r].z, wv[r].w};
+#pragma unroll
+            for (int d = 0; d < 4; ++d) {
+                const uint32_t w0 = wd[d], w8 = wd[d] >> 8;
+                dec[r][4 * d + 0] = (w0 ^ Q4_SIGN) & Q4_LO;
+                dec[r][4 * d + 1] = (w0 ^ Q4_SIGN) & Q4_HI;
+                dec[r][4 * d + 2] = (w8 ^ Q4_SIGN) & Q4_LO;
+                dec[r][4 * d + 3] = (w8 ^ Q4_SIGN) & Q4_HI;
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+            Q4X q;
+            q4_prep(xv[t], q);
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                float se = 0.f, so = 0.f;
+#pragma unroll
+                for (int d = 0; d < 4; ++d) {
+                    se = dot2<FMT_F16>(dec[r][4 * d + 0], q.p[4 * d + 0], se);
+                    so = dot2<FMT_F16>(dec[r][4 * d + 1], q.p[4 * d + 1], so);
+                    se = dot2<FMT_F16>(dec[r][4 * d + 2], q.p[4 * d + 2], se);
+                    so = dot2<FMT_F16>(dec[r][4 * d + 3], q.p[4 * d + 3], so);
+                }
+                const float blk = __builtin_fmaf(so, 0.0625f, se) - q.off;
+                acc[t * R + r] = __builtin_fmaf(f16_bits_to_f32(sv[r]), blk, acc[t * R + r]);
+            }
+        }
+    }
+    wave_sum_entries<N>(acc, lane);
+    if constexpr (N <= WAVE) {
+        if ((lane & (WAVE / N - 1)) == 0) {
+            const int e = lane / (WAVE / N);
+            y[(e / R) * ycs + i + e % R] = acc[0] * 16777216.0f;   /* undo the 2^-24 unit (exact) */
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < N / WAVE; ++j) {
+            const int e = lane * (N / WAVE) + j;
+            y[(e / R) * ycs + i + e % R] = acc[j] * 16777216.0f;
+        }
+    }
+}
+
+/* Rows per wave of the multi-column q4 loop for T = 1, 2, 4, 8 columns (the T raw activation
+   blocks and R decoded rows stay in registers, so T stops at 8). */
+template <int T> struct Cols4 { static constexpr int R = 8; };
+template <> struct Cols4<4> { static constexpr int R = 4; };
+template <> struct Cols4<8> { static constexpr int R = 4; };
+
+/* Rows [r0, r1) of a q4 matrix for tokens token0 .. token0 + T - 1 in one pass over the codes. */
+template <int T, int R = Cols4<T>::R>
+__device__ __forceinline__ void rows_q4_cols(const DevMat& d, int64_t r0, int64_t r1, int32_t token0,
+                                             int lane) {
+    static_assert(T <= 8, "q4 takes at most 8 columns per pass");
+    g_u32x4* Wq = as_global<g_u32x4*>(d.w);
+    g_u16* S = as_global<g_u16*>(d.s);
+    g_u32x4* x = as_global<g_u32x4*>(static_cast<const char*>(d.x) + token0 * d.x_stride);
+    g_f32* y = as_global<g_f32*>(reinterpret_cast<char*>(d.y) + token0 * d.y_stride);
+    const int64_t xcs = d.x_stride / 16, ycs = d.y_stride / 4;
+    int64_t i = r0;
+    for (; i + R <= r1; i += R) q4_group_cols<R, T>(Wq, S, x, xcs, y, ycs, d.nc, i, lane);
+    for (; i < r1; ++i) q4_group_cols<1, T>(Wq, S, x, xcs, y, ycs, d.nc, i, lane);
+}
+
 /* Rows [r0, r1) of a q4 matrix.  With NB >= 2, when rows hold whole steps (nb a multiple of 64 U),
    the units (group of R rows, step) run as one software pipeline over NB register sets: the loads
    of the NB - 1 units after the current one are in flight while it is decoded.  The main loop is
@@ -580,7 +681,7 @@ __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, con
         /* A byte boundary maps to the first row group starting at or after it, the same way for
            the ranges on both sides, so the ranges still cover each row once and break only
            between whole groups of R rows. */
-        const int64_t g = fmt == FMT_Q4 ? RQ : (T == 1 ? R16 : RC);
+        const int64_t g = fmt == FMT_Q4 ? (T == 1 ? RQ : Cols4<(T <= 8 ? T : 8)>::R) : (T == 1 ? R16 : RC);
         const int64_t r0 = lo > d.cost0 ? ceil_div(lo - d.cost0, d.row_bytes * g) * g : 0;
         const int64_t e1 = ceil_div(hi - d.cost0, d.row_bytes * g) * g;
         const int64_t r1 = d.M < e1 ? d.M : e1;
@@ -597,6 +698,9 @@ __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, con
                 rows16_cols<FMT_F16, T, RC, UC>(d, r0, r1, token, lane);
             else if ((FMT == 0 || FMT == FMT_BF16) && fmt == FMT_BF16)
                 rows16_cols<FMT_BF16, T, RC, UC>(d, r0, r1, token, lane);
+            else if constexpr (T <= 8) {
+                if ((FMT == 0 || FMT == FMT_Q4) && fmt == FMT_Q4) rows_q4_cols<T>(d, r0, r1, token, lane);
+            }
         }
     }
 }

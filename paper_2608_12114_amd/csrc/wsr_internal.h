@@ -35,14 +35,14 @@ hipError_t launch_probe(const float* buf, int64_t n, double* sum_dev, void* ws, 
 int64_t probe_grid(int64_t n);
 
 hipError_t launch_gemv(const DevMat& m, hipStream_t s);
-/* T (1, 2, 4, 8 or 16) activation columns per weight read; 16-bit formats only.  m.x_stride and
-   m.y_stride are the column strides in bytes. */
+/* T activation columns per weight read (1, 2, 4, 8 or 16 for 16-bit formats, up to 8 for q4).
+   m.x_stride and m.y_stride are the column strides in bytes. */
 hipError_t launch_gemv_cols(const DevMat& m, int T, hipStream_t s);
 /* Writes the table and clears the two tile counters at ctr (ctr may be null). */
 hipError_t launch_put_table(DevMat* dst, int64_t* cost, const DevMat* src, int n, unsigned* ctr,
                             hipStream_t s);
-/* One pass over the table's weights for tokens token .. token + T - 1 (T = 1, 2, 4, 8, 16).  With
-   T > 1 the table must hold no q4 matrix: the multi-column path covers the 16-bit formats only. */
+/* One pass over the table's weights for tokens token .. token + T - 1 (T = 1, 2, 4, 8, 16; at most
+   8 when the table holds a q4 matrix). */
 hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, int nmat, int64_t total_bytes,
                         int fmt_all, int32_t token, int T, unsigned* ctr, hipStream_t s);
 

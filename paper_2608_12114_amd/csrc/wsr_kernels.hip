@@ -167,10 +167,29 @@ static hipError_t launch_gemv16_cols(const DevMat& m, int T, hipStream_t s) {
     }
 }
 
+template <int T>
+__global__ __launch_bounds__(BLOCK) void k_gemv_q4_cols(DevMat d) {
+    constexpr int R = Cols4<T>::R;
+    const int lane = threadIdx.x & (WAVE - 1);
+    const int64_t wave = (int64_t)blockIdx.x * WAVES_PER_BLOCK + wave_in_block();
+    const int64_t r0 = wave * R;
+    if (r0 >= d.M) return;
+    rows_q4_cols<T>(d, r0, std::min<int64_t>(r0 + R, d.M), 0, lane);
+}
+
 hipError_t launch_gemv_cols(const DevMat& m, int T, hipStream_t s) {
     if (m.M == 0) return hipSuccess;
     if (m.fmt == FMT_F16) return launch_gemv16_cols<FMT_F16>(m, T, s);
     if (m.fmt == FMT_BF16) return launch_gemv16_cols<FMT_BF16>(m, T, s);
+    if (m.fmt == FMT_Q4) {
+        switch (T) {
+            case 1: return launch_rows(k_gemv_q4_cols<1>, m, Cols4<1>::R, s);
+            case 2: return launch_rows(k_gemv_q4_cols<2>, m, Cols4<2>::R, s);
+            case 4: return launch_rows(k_gemv_q4_cols<4>, m, Cols4<4>::R, s);
+            case 8: return launch_rows(k_gemv_q4_cols<8>, m, Cols4<8>::R, s);
+            default: return hipErrorInvalidValue;
+        }
+    }
     return hipErrorInvalidValue;
 }
 
@@ -332,14 +351,23 @@ hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, int nmat, int64_
                         int32_t token, int T, unsigned* ctr, hipStream_t s) {
     if (nmat == 0 || total == 0) return hipSuccess;
     if (fmt_all == FMT_Q4) {
-        if (T != 1) return hipErrorInvalidValue;
         /* About SWEEP_SPAN_Q4 bytes per wave, at least one wave per SIMD. */
         const int64_t waves = std::max<int64_t>((int64_t)cu_count() * WAVES_PER_BLOCK,
                                                 (total + SWEEP_SPAN_Q4 - 1) / SWEEP_SPAN_Q4);
         const int64_t blocks = (waves + WAVES_PER_BLOCK - 1) / WAVES_PER_BLOCK;
         if (blocks > INT32_MAX) return hipErrorInvalidValue;
-        hipLaunchKernelGGL((k_sweep<FMT_Q4, SCHED_SPANS, 4, 4, 8, 1>), dim3((unsigned)blocks), dim3(BLOCK), 0, s,
-                           tab, cost, nmat, total, (int64_t)0, (int64_t)0, token, ctr);
+        const dim3 g((unsigned)blocks);
+#define WSR_Q4_SWEEP(TT)                                                                                      \
+    hipLaunchKernelGGL((k_sweep<FMT_Q4, SCHED_SPANS, 4, 4, 8, 1, 2, TT>), g, dim3(BLOCK), 0, s, tab, cost, nmat, \
+                       total, (int64_t)0, (int64_t)0, token, ctr)
+        switch (T) {
+            case 1: WSR_Q4_SWEEP(1); break;
+            case 2: WSR_Q4_SWEEP(2); break;
+            case 4: WSR_Q4_SWEEP(4); break;
+            case 8: WSR_Q4_SWEEP(8); break;
+            default: return hipErrorInvalidValue;
+        }
+#undef WSR_Q4_SWEEP
         return hipGetLastError();
     }
     const dim3 grid((unsigned)(cu_count() * SWEEP_BLOCKS_PER_CU_16));
@@ -347,7 +375,7 @@ hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, int nmat, int64_
     switch (fmt_all) {
         case FMT_F16: return launch_sweep_cols<FMT_F16>(grid, T, s, tab, cost, nmat, total, tile, token, ctr);
         case FMT_BF16: return launch_sweep_cols<FMT_BF16>(grid, T, s, tab, cost, nmat, total, tile, token, ctr);
-        default:   /* mixed formats; with T > 1 the caller has checked that none is q4 */
+        default:   /* mixed formats; a table holding q4 comes with T <= 8 */
             return launch_sweep_cols<0>(grid, T, s, tab, cost, nmat, total, tile, token, ctr);
     }
 }

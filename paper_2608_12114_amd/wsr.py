@@ -62,8 +62,10 @@ _L.wsr_sweep_workspace_bytes.restype = _sz
 _L.wsr_decode_sweep.argtypes = [ctypes.POINTER(wsr_mat), _i32, _i32, _vp, _sz, _vp]
 _L.wsr_gemv_f16_cols.argtypes = [_vp, _vp, _i64, _vp, _i64, _i64, _i64, _i32, ctypes.c_int, _vp]
 _L.wsr_decode_sweep_batched.argtypes = [ctypes.POINTER(wsr_mat), _i32, _i32, _i32, _vp, _sz, _vp]
+_L.wsr_gemv_q4_cols.argtypes = [_vp, _vp, _vp, _i64, _vp, _i64, _i64, _i64, _i32, _vp]
 for _f in ("wsr_register_host", "wsr_unregister_host", "wsr_probe_read", "wsr_gemv_f16",
-           "wsr_gemv_q4", "wsr_decode_sweep", "wsr_gemv_f16_cols", "wsr_decode_sweep_batched"):
+           "wsr_gemv_q4", "wsr_decode_sweep", "wsr_gemv_f16_cols", "wsr_decode_sweep_batched",
+           "wsr_gemv_q4_cols"):
     getattr(_L, _f).restype = ctypes.c_int
 
 
@@ -127,6 +129,12 @@ def wsr_gemv_f16_cols(W, x, x_col_stride: int, y, y_col_stride: int, M: int, K: 
                       stream=None) -> None:
     _check(_L.wsr_gemv_f16_cols(_ptr(W), _ptr(x), x_col_stride, _ptr(y), y_col_stride, M, K, T, fmt,
                                 _stream(stream)))
+
+
+def wsr_gemv_q4_cols(Wq, scales, x, x_col_stride: int, y, y_col_stride: int, M: int, K: int, T: int,
+                     stream=None) -> None:
+    _check(_L.wsr_gemv_q4_cols(_ptr(Wq), _ptr(scales), _ptr(x), x_col_stride, _ptr(y), y_col_stride, M, K, T,
+                               _stream(stream)))
 
 
 def wsr_gemv_q4(Wq, scales, x, y, M: int, K: int, stream=None) -> None:

@@ -21,7 +21,7 @@ def declared():
 
 def test_exports_every_declared_symbol():
     names = declared()
-    assert len(names) == 12, names
+    assert len(names) == 13, names
     for n in names:
         assert hasattr(L, n), n
 
@@ -90,6 +90,18 @@ def test_gemv_cols_argument_checks():
     assert _status(f, None, None, 0, None, 0, 0, 8, 4, 1, None) == wsr.WSR_OK      # M = 0
 
 
+def test_gemv_q4_cols_argument_checks():
+    f = "wsr_gemv_q4_cols"
+    # (Wq, scales, x, x_col_stride, y, y_col_stride, M, K, T, stream)
+    for T in (0, 3, 16, -4):
+        assert _status(f, A, A, A, 64, A, 64, 4, 64, T, None) == wsr.WSR_E_ARG, T   # 1, 2, 4 or 8
+    assert _status(f, A, None, A, 64, A, 64, 4, 64, 2, None) == wsr.WSR_E_ARG       # no scales
+    assert _status(f, A, A, A, 64, A, 64, 4, 48, 2, None) == wsr.WSR_E_ALIGN        # K % 32
+    assert _status(f, A, A, A, 72, A, 64, 4, 64, 2, None) == wsr.WSR_E_ALIGN        # x stride % 16
+    assert _status(f, A, A, A, 64, A, 8, 4, 64, 2, None) == wsr.WSR_E_ARG           # output columns overlap
+    assert _status(f, None, None, None, 0, None, 0, 0, 64, 8, None) == wsr.WSR_OK   # M = 0
+
+
 def test_batched_sweep_argument_checks():
     good = dict(fmt=2, M=8, K=64, w=A, x=A, y=A, x_tok_stride=128, y_tok_stride=32)
     mats = wsr.make_mats([good, good])
@@ -97,9 +109,8 @@ def test_batched_sweep_argument_checks():
     f = "wsr_decode_sweep_batched"
     for b in (0, 3, 32, -2):
         assert _status(f, mats, 2, 4, b, A, ws, None) == wsr.WSR_E_ARG, b
-    q = wsr.make_mats([good, dict(good, fmt=3, scales=A)])
-    assert _status(f, q, 2, 4, 2, A, ws, None) == wsr.WSR_E_UNSUPPORTED            # q4 takes batch 1
-    assert "batch 1" in wsr.wsr_last_error()
+    q = wsr.make_mats([good, dict(good, fmt=3, scales=A, y_tok_stride=16)])
+    assert _status(f, q, 2, 4, 16, A, ws, None) == wsr.WSR_E_ARG                  # q4 outputs overlap too
     shared = wsr.make_mats([good, dict(good, y_tok_stride=0)])
     assert _status(f, shared, 2, 4, 2, A, ws, None) == wsr.WSR_E_ARG               # tokens would share y
     assert _status(f, mats, 2, 0, 2, A, ws, None) == wsr.WSR_E_ARG                 # n_tokens < 1

@@ -94,3 +94,41 @@ def test_batched_sweep_parity(model16):
         for t in (0, 15, 20):
             want = ora.gemv16(model16.host_weights(i), model16.host_x(i, t), fmt, threads=8)
             assert rel_l2(ys[i][t], want) <= TOL, (m.name, m.layer, t)
+
+
+def single_q4(Wq, S, x, M, K):
+    y = torch.full((max(M, 1),), float("nan"), dtype=torch.float32, device="cuda")
+    wsr.wsr_gemv_q4(Wq, S, x, y, M, K, stream())
+    return y[:M].cpu().numpy()
+
+
+@pytest.mark.parametrize("T", [1, 2, 4, 8])
+@pytest.mark.parametrize("M,K", [(37, 512), (258, 4096), (300, 14336), (5, 32), (9, 2080)])
+def test_q4_cols_parity_and_bitwise(T, M, K):
+    Wqh = synth.q4_codes(M, K, seed=5, stream=311)
+    Sh = synth.q4_scales(M, K, seed=5, stream=312)
+    Xh = synth.normal16((T, K), wl.X_SIGMA, "f16", seed=5, stream=313)
+    Wq, S, X = dv.to_device(Wqh), dv.to_device(Sh), dv.to_device(Xh)
+    Y = torch.full((T, M), float("nan"), dtype=torch.float32, device="cuda")
+    wsr.wsr_gemv_q4_cols(Wq, S, X, K * 2, Y, M * 4, M, K, T, stream())
+    Y = Y.cpu().numpy()
+    ora = oracle.get()
+    for t in range(T):
+        assert rel_l2(Y[t], ora.gemv_q4(Wqh, Sh, Xh[t], threads=8)) <= TOL, t
+        assert np.array_equal(f32_bits(Y[t]), f32_bits(single_q4(Wq, S, X[t], M, K))), t
+
+
+@pytest.fixture(scope="module")
+def model_mixed():
+    mats = wl.decode_matrices(dv.small_model(layers=2, d=512, ffn=1536, vocab=3000))
+    fmts = [(wl.Q4, "bf16", wl.Q4)[m.layer] for m in mats]
+    return dv.SweepInputs(mats, fmts, tokens=13)
+
+
+@pytest.mark.parametrize("batch", [2, 4, 8, 16])
+def test_batched_sweep_with_q4_equals_sequential(model_mixed, batch):
+    """q4 and bf16 matrices in one table; batch 16 runs as passes of 8."""
+    seq = run(model_mixed, 13, None)
+    bat = run(model_mixed, 13, batch)
+    for a, b in zip(seq, bat):
+        assert np.array_equal(f32_bits(a), f32_bits(b))
