@@ -149,7 +149,8 @@ def run_sweep(name, steps, warmup, stream, wsr, want_cpu, cpu_seconds, passes=4)
         f"{gbps:.1f} GB/s ({gbps * 1e9 / HBM_PEAK * 100:.1f}% of 8 TB/s), {1 / per_tok:.2f} tok/s")
     parity = check_sweep(inp, [0, steps - 1])
     log(f"{name}: parity on sampled rows: worst rel-L2 {parity['worst_rel_l2']:.2e}")
-    batched = batch_sweep(name, inp, specs, ws, steps, bpt, stream, wsr) if fmt != wl.Q4 else None
+    batched = batch_sweep(name, inp, specs, ws, steps, bpt, stream, wsr,
+                          (1, 2, 4, 8) if fmt == wl.Q4 else (1, 2, 4, 8, 16))
     out = {"workload": name, "bytes_per_token": bpt, "footprint_bytes": wl.footprint_bytes(shape, fmt),
            "tokens_timed": steps, "warmup_tokens": warmup, "ms_per_token": per_tok * 1e3,
            "GBps": gbps, "hbm_frac": gbps * 1e9 / HBM_PEAK, "tokens_per_s": 1 / per_tok,

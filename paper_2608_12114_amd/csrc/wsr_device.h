@@ -566,10 +566,13 @@ __device__ __forceinline__ void q4_group_cols(g_u32x4* Wq, g_u16* S, g_u32x4* x,
 }
 
 /* Rows per wave of the multi-column q4 loop for T = 1, 2, 4, 8 columns (the T raw activation
-   blocks and R decoded rows stay in registers, so T stops at 8). */
+   blocks and R decoded rows stay in registers, so T stops at 8).  A 16-byte code block needs 64
+   bytes of activations per column, so a step reloads 4 T / R activation bytes (from L2) per code
+   byte; with registers for only R T sums, that traffic, not HBM, sets the rate of these passes. */
 template <int T> struct Cols4 { static constexpr int R = 8; };
+template <> struct Cols4<2> { static constexpr int R = 4; };
 template <> struct Cols4<4> { static constexpr int R = 4; };
-template <> struct Cols4<8> { static constexpr int R = 4; };
+template <> struct Cols4<8> { static constexpr int R = 2; };
 
 /* Rows [r0, r1) of a q4 matrix for tokens token0 .. token0 + T - 1 in one pass over the codes. */
 template <int T, int R = Cols4<T>::R>
@@ -658,7 +661,7 @@ __device__ __forceinline__ void rows_q4(const DevMat& d, int64_t r0, int64_t r1,
 __device__ __forceinline__ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 template <int FMT, int R16, int U16, int RQ, int UQ, int QNB = 2, int T = 1, int RC = Cols16<T>::R,
-          int UC = Cols16<T>::U>
+          int UC = Cols16<T>::U, int RQC = Cols4<(T <= 8 ? T : 8)>::R>
 __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, const int64_t* __restrict__ cost,
                                              int nmat, int64_t lo, int64_t hi, int32_t token, int lane,
                                              int& hint) {
@@ -681,7 +684,7 @@ __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, con
         /* A byte boundary maps to the first row group starting at or after it, the same way for
            the ranges on both sides, so the ranges still cover each row once and break only
            between whole groups of R rows. */
-        const int64_t g = fmt == FMT_Q4 ? (T == 1 ? RQ : Cols4<(T <= 8 ? T : 8)>::R) : (T == 1 ? R16 : RC);
+        const int64_t g = fmt == FMT_Q4 ? (T == 1 ? RQ : RQC) : (T == 1 ? R16 : RC);
         const int64_t r0 = lo > d.cost0 ? ceil_div(lo - d.cost0, d.row_bytes * g) * g : 0;
         const int64_t e1 = ceil_div(hi - d.cost0, d.row_bytes * g) * g;
         const int64_t r1 = d.M < e1 ? d.M : e1;
@@ -699,7 +702,7 @@ __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, con
             else if ((FMT == 0 || FMT == FMT_BF16) && fmt == FMT_BF16)
                 rows16_cols<FMT_BF16, T, RC, UC>(d, r0, r1, token, lane);
             else if constexpr (T <= 8) {
-                if ((FMT == 0 || FMT == FMT_Q4) && fmt == FMT_Q4) rows_q4_cols<T>(d, r0, r1, token, lane);
+                if ((FMT == 0 || FMT == FMT_Q4) && fmt == FMT_Q4) rows_q4_cols<T, RQC>(d, r0, r1, token, lane);
             }
         }
     }

@@ -261,7 +261,7 @@ int64_t sweep_tile(int64_t total, int64_t waves) {
    The counters ctr[0] (next tile) and ctr[1] (waves done) start at zero and the last wave to
    finish puts them back to zero for the next launch. */
 template <int FMT, int SCHED, int R16, int U16, int RQ, int UQ, int QNB = 2, int T = 1, int RC = Cols16<T>::R,
-          int UC = Cols16<T>::U>
+          int UC = Cols16<T>::U, int RQC = Cols4<(T <= 8 ? T : 8)>::R>
 __global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab, const int64_t* __restrict__ cost,
                                                  int nmat, int64_t total, int64_t span, int64_t tile,
                                                  int32_t token, unsigned* __restrict__ ctr) {
@@ -274,12 +274,12 @@ __global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab,
         const int64_t q = total / nw, r = total % nw;
         const int64_t lo = q * w + (int64_t)((uint64_t)r * (uint64_t)w / nw);
         const int64_t hi = q * (w + 1) + (int64_t)((uint64_t)r * (uint64_t)(w + 1) / nw);
-        if (lo < hi) stream_range<FMT, R16, U16, RQ, UQ, QNB, T, RC, UC>(tab, cost, nmat, lo, hi, token, lane, hint);
+        if (lo < hi) stream_range<FMT, R16, U16, RQ, UQ, QNB, T, RC, UC, RQC>(tab, cost, nmat, lo, hi, token, lane, hint);
     } else {
         int64_t base = 0;
         if constexpr (SCHED == SCHED_HYBRID) {
             base = span * nw;
-            if (span > 0) stream_range<FMT, R16, U16, RQ, UQ, QNB, T, RC, UC>(tab, cost, nmat, span * w, span * (w + 1),
+            if (span > 0) stream_range<FMT, R16, U16, RQ, UQ, QNB, T, RC, UC, RQC>(tab, cost, nmat, span * w, span * (w + 1),
                                                                    token, lane, hint);
         }
         /* Each wave claims its next tile before working on the current one, so the round trip of
@@ -292,7 +292,7 @@ __global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab,
             if ((int64_t)t >= ntiles) break;
             if (lane == 0) claim = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             const int64_t lo = base + (int64_t)t * tile;
-            stream_range<FMT, R16, U16, RQ, UQ, QNB, T, RC, UC>(tab, cost, nmat, lo, std::min<int64_t>(total, lo + tile),
+            stream_range<FMT, R16, U16, RQ, UQ, QNB, T, RC, UC, RQC>(tab, cost, nmat, lo, std::min<int64_t>(total, lo + tile),
                                                      token, lane, hint);
         }
         if (lane == 0) {
