@@ -58,6 +58,12 @@ def _bind(L: ctypes.CDLL) -> ctypes.CDLL:
     L.ora_dequant_q4.restype = None
     L.ora_gemv_q4.argtypes = [vp, vp, vp, i64, i64, vp, i32]
     L.ora_gemv_q4.restype = None
+    L.ora_int8.argtypes = [ctypes.c_uint]
+    L.ora_int8.restype = i32
+    L.ora_i8_weight.argtypes = [vp, vp, i64, i64, i64]
+    L.ora_i8_weight.restype = dbl
+    L.ora_gemv_i8.argtypes = [vp, vp, vp, i64, i64, vp, i32]
+    L.ora_gemv_i8.restype = None
     return L
 
 
@@ -103,6 +109,24 @@ class Oracle:
         self.L.ora_dequant_q4(Wq.ctypes.data, S.ctypes.data, M, K, w.ctypes.data)
         return w
 
+    def int8(self, byte: int) -> int:
+        return self.L.ora_int8(byte)
+
+    def i8_weight(self, Wq: np.ndarray, S: np.ndarray, i: int, k: int) -> float:
+        Wq = np.ascontiguousarray(Wq).view(np.uint8)
+        S = np.ascontiguousarray(S, dtype=np.uint16)
+        return self.L.ora_i8_weight(Wq.ctypes.data, S.ctypes.data, Wq.shape[1], i, k)
+
+    def gemv_i8(self, Wq: np.ndarray, S: np.ndarray, x: np.ndarray, threads: int = 1) -> np.ndarray:
+        Wq = np.ascontiguousarray(Wq).view(np.uint8)
+        S = np.ascontiguousarray(S, dtype=np.uint16)
+        x = np.ascontiguousarray(x, dtype=np.uint16)
+        M, K = Wq.shape
+        assert S.shape == (M,) and x.shape == (K,)
+        y = np.empty(M, dtype=np.float64)
+        self.L.ora_gemv_i8(Wq.ctypes.data, S.ctypes.data, x.ctypes.data, M, K, y.ctypes.data, threads)
+        return y
+
     def gemv_q4(self, Wq: np.ndarray, S: np.ndarray, x: np.ndarray, threads: int = 1) -> np.ndarray:
         Wq = np.ascontiguousarray(Wq, dtype=np.uint8)
         S = np.ascontiguousarray(S, dtype=np.uint16)
@@ -115,9 +139,11 @@ class Oracle:
         return y
 
     def gemv(self, mat: dict, x: np.ndarray, threads: int = 1) -> np.ndarray:
-        """GEMV of one sweep matrix: mat = {"fmt": "f16"|"bf16"|"q4", "w": ..., "s": ...}."""
+        """GEMV of one sweep matrix: mat = {"fmt": "f16"|"bf16"|"q4"|"i8", "w": ..., "s": ...}."""
         if mat["fmt"] == "q4":
             return self.gemv_q4(mat["w"], mat["s"], x, threads)
+        if mat["fmt"] == "i8":
+            return self.gemv_i8(mat["w"], mat["s"], x, threads)
         return self.gemv16(mat["w"], x, mat["fmt"], threads)
 
     # -- decode sweep --

@@ -16,6 +16,9 @@
  *                                                      matrix with strides (K, 1), Alg. 1)
  *   q4 dequant w[i,k] = q[i,k] * s[i, floor(k / 32)]  (32 signed int4 codes share one fp16 scale)
  *   gemv_q4    y_i = sum_k w[i,k] * x[k]
+ *   i8 dequant w[i,k] = q[i,k] * s[i]                 (the paper's packed int8 weights with fp16 row
+ *                                                      scales, Sec. 3.1)
+ *   gemv_i8    y_i = sum_k w[i,k] * x[k]
  * Build: gcc -O2 -ffp-contract=off -fPIC -shared -fopenmp (no fast-math, no contraction).
  */
 #include <math.h>
@@ -54,6 +57,12 @@ double ora_bf16_to_f64(uint16_t b) {
 }
 
 /* Signed int4 in two's complement: codes 0..7 are 0..7, codes 8..15 are -8..-1. */
+/* Two's-complement int8 from its byte. */
+int ora_int8(unsigned byte) {
+    byte &= 0xFF;
+    return byte >= 128 ? (int)byte - 256 : (int)byte;
+}
+
 int ora_int4(unsigned code) {
     code &= 0xF;
     return code >= 8 ? (int)code - 16 : (int)code;
@@ -112,6 +121,23 @@ void ora_gemv_q4(const uint8_t* Wq, const uint16_t* S, const uint16_t* x, int64_
     for (int64_t i = 0; i < M; ++i) {
         double acc = 0.0;
         for (int64_t k = 0; k < K; ++k) acc += ora_q4_weight(Wq, S, K, i, k) * ora_f16_to_f64(x[k]);
+        y[i] = acc;
+    }
+}
+
+/* int8 weights with one fp16 scale per row (Sec. 3.1): Wq (M, K) bytes row-major, S[M]. */
+double ora_i8_weight(const uint8_t* Wq, const uint16_t* S, int64_t K, int64_t i, int64_t k) {
+    int q = ora_int8(Wq[i * K + k]);
+    double row_scale = ora_f16_to_f64(S[i]);
+    return (double)q * row_scale;
+}
+
+void ora_gemv_i8(const uint8_t* Wq, const uint16_t* S, const uint16_t* x, int64_t M, int64_t K,
+                 double* y, int threads) {
+#pragma omp parallel for schedule(static) num_threads(threads > 0 ? threads : 1)
+    for (int64_t i = 0; i < M; ++i) {
+        double acc = 0.0;
+        for (int64_t k = 0; k < K; ++k) acc += ora_i8_weight(Wq, S, K, i, k) * ora_f16_to_f64(x[k]);
         y[i] = acc;
     }
 }

@@ -23,6 +23,9 @@ LIB_PATH = os.path.join(_HERE, "libsynth.so")
 SRC_PATH = os.path.join(_HERE, "synth.c")
 
 F16, BF16 = 1, 2
+# int8 row scales ~ U[2.5e-4, 1e-3): the scale max|w| / 127 of a symmetric int8 quantisation of an
+# N(0, 0.02) row of a few thousand weights (max |w| about 4 sigma) is about 6e-4.
+I8_SCALE_LO, I8_SCALE_HI = 2.5e-4, 1e-3
 _FMT = {"f16": F16, "bf16": BF16, F16: F16, BF16: BF16}
 
 
@@ -67,6 +70,9 @@ def lib() -> ctypes.CDLL:
         L.synth_grid.restype = ctypes.c_float
         L.synth_int4.argtypes = [u64, u64, u64]
         L.synth_int4.restype = i32
+        L.synth_int8.argtypes = [u64, u64, u64]
+        L.synth_int8.restype = i32
+        L.synth_i8.argtypes = [vp, i64, u64, u64, u64, i32]
         L.synth_table_bytes.argtypes = []
         L.synth_table_bytes.restype = ctypes.c_size_t
         L.synth_table_build.argtypes = [vp, i32, dbl]
@@ -78,7 +84,7 @@ def lib() -> ctypes.CDLL:
         L.synth_q4.argtypes = [vp, i64, u64, u64, u64, i32]
         L.synth_uniform16.argtypes = [vp, i64, u64, u64, u64, dbl, dbl, i32, i32]
         L.synth_encode16.argtypes = [vp, vp, i64, i32]
-        for f in ("synth_normal16", "synth_grid_f32", "synth_q4",
+        for f in ("synth_normal16", "synth_grid_f32", "synth_q4", "synth_i8",
                   "synth_uniform16", "synth_encode16"):
             getattr(L, f).restype = None
         _lib = L
@@ -155,6 +161,22 @@ def q4_scales(M, K, lo=0.005, hi=0.02, seed=0, stream=0, row0=0, out=None, threa
     assert K % 32 == 0
     nb = K // 32
     return uniform16((M, nb), lo, hi, F16, seed, stream, row0 * nb, out, threads)
+
+
+def i8_codes(M, K, seed=0, stream=0, row0=0, out=None, threads=None):
+    """Signed int8 codes of rows [row0, row0 + M) of a (*, K) matrix, int8 (M, K)."""
+    a = _out(out, (M, K), np.int8)
+    lib().synth_i8(a.ctypes.data, a.size, seed, stream, row0 * K, threads or default_threads())
+    return a
+
+
+def i8_scales(M, lo=I8_SCALE_LO, hi=I8_SCALE_HI, seed=0, stream=0, row0=0, out=None, threads=None):
+    """fp16 row scales of rows [row0, row0 + M) of an int8 matrix, uint16 (M,)."""
+    return uniform16((M,), lo, hi, F16, seed, stream, row0, out, threads)
+
+
+def int8(seed, stream, e):
+    return lib().synth_int8(seed, stream, e)
 
 
 def encode16(values, fmt):

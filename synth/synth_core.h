@@ -108,6 +108,9 @@ SYNTH_FN uint8_t synth_q4_byte(uint64_t seed, uint64_t stream, uint64_t e0, int6
     return (uint8_t)((lo & 0xF) | ((hi & 0xF) << 4));
 }
 
+/* Signed int8 uniform on {-128..127}: top 8 bits of the draw minus 128. */
+SYNTH_FN int8_t synth_int8_value(uint64_t u) { return (int8_t)((int)(u >> 56) - 128); }
+
 /* Uniform on [lo, hi), rounded to fp16 / bf16. */
 SYNTH_FN uint16_t synth_uniform16_value(uint64_t u, double lo, double hi, int fmt) {
     return synth_enc16(lo + (hi - lo) * synth_top53(u), fmt);

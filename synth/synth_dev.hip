@@ -39,6 +39,14 @@ __global__ __launch_bounds__(BLOCK) void k_q4(uint8_t* __restrict__ out, int64_t
         for (int j = 0; j < PER && i + j < nbytes; ++j) out[i + j] = synth_q4_byte(seed, stream, e0, i + j);
 }
 
+__global__ __launch_bounds__(BLOCK) void k_i8(int8_t* __restrict__ out, int64_t n, uint64_t seed,
+                                              uint64_t stream, uint64_t e0) {
+    const int64_t step = (int64_t)gridDim.x * BLOCK * PER;
+    for (int64_t i = ((int64_t)blockIdx.x * BLOCK + threadIdx.x) * PER; i < n; i += step)
+        for (int j = 0; j < PER && i + j < n; ++j)
+            out[i + j] = synth_int8_value(synth_draw(seed, stream, e0 + (uint64_t)(i + j)));
+}
+
 __global__ __launch_bounds__(BLOCK) void k_grid(float* __restrict__ out, int64_t n, uint64_t seed,
                                                 uint64_t stream, uint64_t e0) {
     const int64_t step = (int64_t)gridDim.x * BLOCK * PER;
@@ -76,6 +84,12 @@ int synth_dev_q4(uint8_t* out, int64_t nbytes, uint64_t seed, uint64_t stream, u
     if (nbytes <= 0) return 0;
     hipLaunchKernelGGL(k_q4, dim3(grid_for(nbytes)), dim3(BLOCK), 0, (hipStream_t)s, out, nbytes, seed,
                        stream, e0);
+    return (int)hipGetLastError();
+}
+
+int synth_dev_i8(int8_t* out, int64_t n, uint64_t seed, uint64_t stream, uint64_t e0, void* s) {
+    if (n <= 0) return 0;
+    hipLaunchKernelGGL(k_i8, dim3(grid_for(n)), dim3(BLOCK), 0, (hipStream_t)s, out, n, seed, stream, e0);
     return (int)hipGetLastError();
 }
 

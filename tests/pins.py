@@ -269,12 +269,73 @@ def pin_q4_column_invariant(ora):
     assert abs(lhs - rhs) <= (M + K) * 2.0 ** -52 * float(np.abs(w * xd).sum())
 
 
+# ---- int8 with fp16 row scales ----------------------------------------------------------------------
+
+def pin_int8_table(ora):
+    """All 256 bytes against numpy's two's-complement reinterpretation."""
+    ref = np.arange(256, dtype=np.uint16).astype(np.uint8).view(np.int8)
+    for b in range(256):
+        assert ora.int8(b) == int(ref[b]), f"byte {b:#04x}"
+
+
+def _i8(M, K, seed):
+    return synth.i8_codes(M, K, seed=seed, stream=21), synth.i8_scales(M, seed=seed, stream=22)
+
+
+def pin_i8_units(ora):
+    M, K = 13, 80
+    Wq, S = _i8(M, K, 81)
+    q, s = Wq.astype(np.float64), _f16_ref(S)
+    zero, one = synth.encode16([0.0, 1.0], "f16")
+    for j in (0, 1, 15, 16, 17, 63, K - 1):
+        e = np.full(K, zero, np.uint16)
+        e[j] = one
+        assert np.array_equal(ora.gemv_i8(Wq, S, e), q[:, j] * s), j
+    assert ora.i8_weight(Wq, S, 3, 7) == q[3, 7] * s[3]
+
+
+def pin_i8_row_scales(ora):
+    """Every weight 1 and distinct scales per row: y_i = s_i * sum(x), exactly in rationals."""
+    M, K = 9, 48
+    Wq = np.ones((M, K), np.int8)
+    S = synth.encode16([0.5 + 0.125 * i for i in range(M)], "f16")
+    x = _rand16(K, "f16", 82, 3)
+    xs = sum((Fraction(float(v)) for v in _f16_ref(x)), Fraction(0))
+    y = ora.gemv_i8(Wq, S, x)
+    for i in range(M):
+        assert abs(y[i] - float(Fraction(float(_f16_ref(S)[i])) * xs)) <= K * 2.0 ** -50, i
+
+
+def pin_i8_brute_force(ora):
+    for (M, K, seed) in ((4, 48, 1), (7, 16, 2), (3, 112, 3)):
+        Wq, S = _i8(M, K, 83 + seed)
+        x = _rand16(K, "f16", seed, 19)
+        q, s, xd = Wq.astype(np.int64), _f16_ref(S), _f16_ref(x)
+        y = ora.gemv_i8(Wq, S, x)
+        for i in range(M):
+            exact = sum((Fraction(int(q[i, k])) * Fraction(float(s[i])) * Fraction(float(xd[k]))
+                         for k in range(K)), Fraction(0))
+            bound = K * 2.0 ** -53 * float(np.abs(q[i] * s[i] * xd).sum()) + 1e-300
+            assert abs(y[i] - float(exact)) <= bound, (M, K, i)
+
+
+def pin_i8_column_invariant(ora):
+    M, K = 19, 64
+    Wq, S = _i8(M, K, 87)
+    x = _rand16(K, "f16", 87, 2)
+    w, xd = Wq.astype(np.float64) * _f16_ref(S)[:, None], _f16_ref(x)
+    col = [sum((Fraction(float(w[i, k])) for i in range(M)), Fraction(0)) for k in range(K)]
+    rhs = float(sum((col[k] * Fraction(float(xd[k])) for k in range(K)), Fraction(0)))
+    lhs = float(sum((Fraction(float(v)) for v in ora.gemv_i8(Wq, S, x)), Fraction(0)))
+    assert abs(lhs - rhs) <= (M + K) * 2.0 ** -52 * float(np.abs(w * xd).sum())
+
+
 # ---- decode sweep ----------------------------------------------------------------------------------
 
 def pin_sweep_tokens_and_order(ora):
     """Two tiny layers plus a head, three tokens, mixed formats: every (token, matrix) output equals
     the exact rational product of that matrix with that token's activation."""
-    shapes = [("bf16", 6, 16), ("bf16", 4, 16), ("q4", 5, 64), ("f16", 3, 24)]
+    shapes = [("bf16", 6, 16), ("bf16", 4, 16), ("q4", 5, 64), ("i8", 3, 32), ("f16", 3, 24)]
     mats, xs = [], []
     for m, (fmt, M, K) in enumerate(shapes):
         if fmt == "q4":
@@ -282,6 +343,11 @@ def pin_sweep_tokens_and_order(ora):
             mats.append({"fmt": fmt, "w": Wq, "s": S})
             q, s = _q4_ref(Wq, S)
             dense = q * s
+            xfmt = "f16"
+        elif fmt == "i8":
+            Wq, S = _i8(M, K, 60 + m)
+            mats.append({"fmt": fmt, "w": Wq, "s": S})
+            dense = Wq.astype(np.float64) * _f16_ref(S)[:, None]
             xfmt = "f16"
         else:
             W = _rand16((M, K), fmt, 60 + m, 1, 0.25)

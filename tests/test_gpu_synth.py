@@ -34,3 +34,12 @@ def test_q4_scales_grid_device_equal_host(nbytes, row0):
     g = torch.empty(nbytes, dtype=torch.float32, device="cuda")
     dv.gen_grid_f32(g, seed=1, stream=11, e0=row0)
     assert np.array_equal(g.cpu().numpy(), synth.grid_f32(nbytes, seed=1, stream=11, e0=row0))
+
+
+@pytest.mark.parametrize("n,e0", [(1, 0), (4099, 7), (1 << 20, 123456789)])
+def test_i8_device_equals_host(n, e0):
+    t = torch.empty(n, dtype=torch.int8, device="cuda")
+    dv.gen_i8(t, seed=2, stream=13, e0=e0)
+    host = np.empty(n, np.int8)
+    synth.lib().synth_i8(host.ctypes.data, n, 2, 13, e0, 4)
+    assert np.array_equal(t.cpu().numpy(), host)

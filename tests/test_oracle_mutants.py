@@ -32,6 +32,13 @@ MUTANTS = {
     "gemvq4_drop_first": ("for (int64_t k = 0; k < K; ++k) acc += ora_q4_weight",
                           "for (int64_t k = 1; k < K; ++k) acc += ora_q4_weight"),
     "gemvq4_no_scale": ("return (double)q * s;", "return (double)q;"),
+    "int8_unsigned": ("byte >= 128 ? (int)byte - 256 : (int)byte", "(int)byte"),
+    "int8_threshold": ("byte >= 128 ? (int)byte - 256", "byte > 128 ? (int)byte - 256"),
+    "i8_first_row_scale": ("double row_scale = ora_f16_to_f64(S[i]);", "double row_scale = ora_f16_to_f64(S[0]);"),
+    "i8_no_scale": ("return (double)q * row_scale;", "return (double)q;"),
+    "i8_columns_reversed": ("ora_int8(Wq[i * K + k])", "ora_int8(Wq[i * K + (K - 1 - k)])"),
+    "gemvi8_drop_last": ("for (int64_t k = 0; k < K; ++k) acc += ora_i8_weight",
+                         "for (int64_t k = 0; k < K - 1; ++k) acc += ora_i8_weight"),
     "probe_drop_last": ("for (int64_t i = 0; i < n; ++i) s += (double)buf[i];",
                         "for (int64_t i = 0; i + 1 < n; ++i) s += (double)buf[i];"),
     "probe_float_accumulate": ("double s = 0.0;\n    for (int64_t i = 0; i < n; ++i) s += (double)buf[i];",

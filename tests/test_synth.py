@@ -142,3 +142,15 @@ def test_int4_uniform():
     codes = np.concatenate([c & 0xF, c >> 4]).ravel()
     counts = np.bincount(codes, minlength=16)
     assert counts.min() > 0.9 * codes.size / 16 and counts.max() < 1.1 * codes.size / 16
+
+
+def test_int8_uniform_and_rows():
+    c = synth.i8_codes(2000, 128, seed=0, stream=3)
+    counts = np.bincount(c.view(np.uint8).ravel(), minlength=256)
+    assert counts.min() > 0.85 * c.size / 256 and counts.max() < 1.15 * c.size / 256
+    assert c.min() == -128 and c.max() == 127
+    part = synth.i8_codes(3, 128, seed=0, stream=3, row0=7)
+    assert np.array_equal(c[7:10], part)
+    assert synth.int8(0, 3, 7 * 128 + 5) == c[7, 5]
+    s = synth.i8_scales(500, seed=0, stream=4).view(np.float16).astype(np.float64)
+    assert s.min() >= synth.I8_SCALE_LO * (1 - 2 ** -10) and s.max() <= synth.I8_SCALE_HI
