@@ -45,7 +45,7 @@ typedef enum {
     WSR_E_ARG = 1,          /* null pointer, negative size, unknown format or flag, n_tokens < 1  */
     WSR_E_ALIGN = 2,        /* host range base or length not a page multiple (Alg. 1's reject
                                rule); device operand misaligned; K % 8 != 0 (16-bit) or
-                               K % 32 != 0 (q4)                                                  */
+                               K % 32 != 0 (q4) or K % 16 != 0 (int8)                            */
     WSR_E_SIZE = 3,         /* workspace too small, or a size whose byte count overflows        */
     WSR_E_UNSUPPORTED = 4,  /* the runtime refused a request, e.g. pinning an existing host range
                                (distinct from a failed HIP call, Sec. 7.3)                      */
@@ -56,7 +56,8 @@ typedef enum {
 typedef enum {
     WSR_F16 = 1,    /* IEEE binary16                                                          */
     WSR_BF16 = 2,   /* bfloat16                                                               */
-    WSR_Q4 = 3      /* blocks of 32 signed int4 weights sharing one fp16 scale (see gemv_q4)   */
+    WSR_Q4 = 3,     /* blocks of 32 signed int4 weights sharing one fp16 scale (see gemv_q4)   */
+    WSR_I8 = 4      /* signed int8 weights with one fp16 scale per row (see gemv_i8)           */
 } wsr_fmt;
 
 /* Message describing the last failed call on this thread ("" if none). */
@@ -123,6 +124,13 @@ wsr_status wsr_gemv_f16(const void* W, const void* x, float* y, int64_t M, int64
 wsr_status wsr_gemv_q4(const uint8_t* Wq, const uint16_t* scales, const uint16_t* x, float* y,
                        int64_t M, int64_t K, void* stream);
 
+/* wsr_gemv_i8: y[i] = s[i] * sum_k q[i,k] * x[k], the matched protocol's weight format (Sec. 3.1:
+   int8 codes with fp16 row scales).  Wq: int8 (M, K) row-major, 16-byte aligned.  scales: fp16
+   bits [M], 2-byte aligned.  x: fp16[K], 16-byte aligned.  y: fp32[M].  K % 16 == 0.  Every
+   product q * x is exact in fp32 and sums are fp32; the row scale multiplies the finished sum. */
+wsr_status wsr_gemv_i8(const int8_t* Wq, const uint16_t* scales, const uint16_t* x, float* y,
+                       int64_t M, int64_t K, void* stream);
+
 /* ---- multi-column GEMV (Sec. 3.4 and 5.2: T activation columns share each weight read) ---------
 
    wsr_gemv_f16_cols: for t < T and i < M, y_t[i] = sum_k W[i*K + k] * x_t[k], where
@@ -142,13 +150,20 @@ wsr_status wsr_gemv_q4_cols(const uint8_t* Wq, const uint16_t* scales, const uin
                             int64_t x_col_stride, float* y, int64_t y_col_stride, int64_t M, int64_t K,
                             int32_t T, void* stream);
 
+/* wsr_gemv_i8_cols: the same for int8 weights (wsr_gemv_i8's layout), T = 1, 2, 4 or 8.  Every
+   y_t is bitwise equal to wsr_gemv_i8(Wq, scales, x_t, y_t, M, K). */
+wsr_status wsr_gemv_i8_cols(const int8_t* Wq, const uint16_t* scales, const uint16_t* x,
+                            int64_t x_col_stride, float* y, int64_t y_col_stride, int64_t M, int64_t K,
+                            int32_t T, void* stream);
+
 /* ---- decode weight sweep ----------------------------------------------------------------------
 
    For t in [0, n_tokens), for m in [0, n) in order: y_m(t) = W_m . x_m(t), where
    x_m(t) = x + t * x_tok_stride bytes and y_m(t) = y + t * y_tok_stride bytes.  One batch-1 token
    reads every matrix once (Sec. 6.2) and a pass over all of them is ordered on the GPU with no
    host synchronisation (Sec. 3.1; C3 of Table 1).  Each matrix follows wsr_gemv_f16 (fmt WSR_F16
-   or WSR_BF16) or wsr_gemv_q4 (WSR_Q4, `scales` set) and their layout and alignment rules.
+   or WSR_BF16), wsr_gemv_q4 (WSR_Q4) or wsr_gemv_i8 (WSR_I8), `scales` set for the last two, and
+   their layout and alignment rules.
    Matrices of one token run in one persistent launch unless a matrix has WSR_MAT_AFTER_PREVIOUS,
    which starts a new launch so that it may read outputs of earlier matrices of the same token.
    ws: at least wsr_sweep_workspace_bytes(mats, n) bytes of device memory, 256-byte aligned; each
@@ -159,8 +174,8 @@ typedef struct wsr_mat {
     int32_t fmt;            /* wsr_fmt                                                    */
     int32_t flags;          /* 0 or WSR_MAT_AFTER_PREVIOUS                                */
     int64_t M, K;
-    const void* w;          /* weights (16-bit) or packed int4 codes (q4)                  */
-    const void* scales;     /* q4 block scales, NULL otherwise                            */
+    const void* w;          /* weights (16-bit), packed int4 codes (q4) or int8 codes      */
+    const void* scales;     /* q4 block scales or int8 row scales, NULL otherwise         */
     const void* x;          /* activation of token 0                                      */
     int64_t x_tok_stride;   /* bytes between tokens' activations (0: same x every token)  */
     float* y;               /* output of token 0                                          */
@@ -176,7 +191,7 @@ wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, vo
    t .. t + batch - 1, whose activations must all be ready when the call is made, as for a batch of
    independent sequences or the candidates of a speculative step (Sec. 3.4, 5.2).  The last
    n_tokens % batch tokens go in passes of the largest power of two that fits.  A table holding a
-   q4 matrix is swept at most 8 tokens per pass (batch 16 acts as 8).  With batch > 1 every matrix
+   q4 or int8 matrix is swept at most 8 tokens per pass (batch 16 acts as 8).  With batch > 1 every matrix
    must have y_tok_stride >= 4 M.  ws as for wsr_decode_sweep. */
 wsr_status wsr_decode_sweep_batched(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch,
                                     void* ws, size_t ws_bytes, void* stream);

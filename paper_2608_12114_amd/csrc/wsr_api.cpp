@@ -57,19 +57,20 @@ std::map<uintptr_t, Reg> g_reg;
 /* Shared validation of one matrix (standalone GEMV or sweep entry). */
 wsr_status check_matrix(int fmt, int64_t M, int64_t K, const void* w, const void* scales,
                         const void* x, const float* y, const char* who) {
-    if (fmt != WSR_F16 && fmt != WSR_BF16 && fmt != WSR_Q4)
+    if (fmt != WSR_F16 && fmt != WSR_BF16 && fmt != WSR_Q4 && fmt != WSR_I8)
         return fail(WSR_E_ARG, "%s: unknown format %d", who, fmt);
     if (M < 0 || K < 0) return fail(WSR_E_ARG, "%s: negative size M=%lld K=%lld", who, (long long)M, (long long)K);
     if (!mul_fits(M, K, 2)) return fail(WSR_E_SIZE, "%s: M*K overflows", who);
-    if (fmt == WSR_Q4 ? (K % 32 != 0) : (K % 8 != 0))
-        return fail(WSR_E_ALIGN, "%s: K=%lld must be a multiple of %d", who, (long long)K, fmt == WSR_Q4 ? 32 : 8);
+    const int kq = fmt == WSR_Q4 ? 32 : fmt == WSR_I8 ? 16 : 8;
+    if (K % kq != 0) return fail(WSR_E_ALIGN, "%s: K=%lld must be a multiple of %d", who, (long long)K, kq);
     if (M == 0) return WSR_OK;
     if (!w || !x || !y) return fail(WSR_E_ARG, "%s: null weight, activation or output pointer", who);
-    if (fmt == WSR_Q4 && !scales) return fail(WSR_E_ARG, "%s: q4 needs scales", who);
+    if ((fmt == WSR_Q4 || fmt == WSR_I8) && !scales) return fail(WSR_E_ARG, "%s: q4 and int8 need scales", who);
     if (!aligned(w, 16) || !aligned(x, 16))
         return fail(WSR_E_ALIGN, "%s: weights and activations must be 16-byte aligned", who);
     if (!aligned(y, 4)) return fail(WSR_E_ALIGN, "%s: output must be 4-byte aligned", who);
-    if (fmt == WSR_Q4 && !aligned(scales, 2)) return fail(WSR_E_ALIGN, "%s: scales must be 2-byte aligned", who);
+    if ((fmt == WSR_Q4 || fmt == WSR_I8) && !aligned(scales, 2))
+        return fail(WSR_E_ALIGN, "%s: scales must be 2-byte aligned", who);
     return WSR_OK;
 }
 
@@ -77,7 +78,7 @@ DevMat make_devmat(int fmt, int64_t M, int64_t K, const void* w, const void* sca
                    float* y) {
     DevMat d{};
     d.w = w;
-    d.s = fmt == WSR_Q4 ? scales : nullptr;
+    d.s = (fmt == WSR_Q4 || fmt == WSR_I8) ? scales : nullptr;
     d.x = x;
     d.y = y;
     d.M = M;
@@ -85,6 +86,9 @@ DevMat make_devmat(int fmt, int64_t M, int64_t K, const void* w, const void* sca
     if (fmt == WSR_Q4) {
         d.nc = K / 32;
         d.row_bytes = K / 2 + (K / 32) * 2;
+    } else if (fmt == WSR_I8) {
+        d.nc = K / 16;
+        d.row_bytes = K + 2;                         /* codes plus the row's scale */
     } else {
         d.nc = K / 8;
         d.row_bytes = K * 2;
@@ -246,6 +250,39 @@ wsr_status wsr_gemv_q4_cols(const uint8_t* Wq, const uint16_t* scales, const uin
     return ok();
 }
 
+wsr_status wsr_gemv_i8(const int8_t* Wq, const uint16_t* scales, const uint16_t* x, float* y,
+                       int64_t M, int64_t K, void* stream) {
+    wsr_status st = check_matrix(WSR_I8, M, K, Wq, scales, x, y, "gemv_i8");
+    if (st != WSR_OK) return st;
+    if (M == 0) return ok();
+    const hipError_t e = wsr::launch_gemv(make_devmat(WSR_I8, M, K, Wq, scales, x, y), static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "gemv_i8: launch");
+    return ok();
+}
+
+wsr_status wsr_gemv_i8_cols(const int8_t* Wq, const uint16_t* scales, const uint16_t* x,
+                            int64_t x_col_stride, float* y, int64_t y_col_stride, int64_t M, int64_t K,
+                            int32_t T, void* stream) {
+    if (T != 1 && T != 2 && T != 4 && T != 8)
+        return fail(WSR_E_ARG, "gemv_i8_cols: T=%d must be 1, 2, 4 or 8", T);
+    wsr_status st = check_matrix(WSR_I8, M, K, Wq, scales, x, y, "gemv_i8_cols");
+    if (st != WSR_OK) return st;
+    if (x_col_stride < 0 || x_col_stride % 16 || y_col_stride < 0 || y_col_stride % 4)
+        return fail(WSR_E_ALIGN, "gemv_i8_cols: column strides must be >= 0 and multiples of 16 (x) and 4 (y)");
+    if (T > 1 && y_col_stride < M * 4)
+        return fail(WSR_E_ARG, "gemv_i8_cols: output columns overlap (y_col_stride %lld < 4 M)",
+                    (long long)y_col_stride);
+    if (!mul_fits(x_col_stride, T) || !mul_fits(y_col_stride, T))
+        return fail(WSR_E_SIZE, "gemv_i8_cols: column strides overflow");
+    if (M == 0) return ok();
+    DevMat d = make_devmat(WSR_I8, M, K, Wq, scales, x, y);
+    d.x_stride = x_col_stride;
+    d.y_stride = y_col_stride;
+    const hipError_t e = wsr::launch_gemv_cols(d, T, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "gemv_i8_cols: launch");
+    return ok();
+}
+
 wsr_status wsr_gemv_q4(const uint8_t* Wq, const uint16_t* scales, const uint16_t* x, float* y,
                        int64_t M, int64_t K, void* stream) {
     wsr_status st = check_matrix(WSR_Q4, M, K, Wq, scales, x, y, "gemv_q4");
@@ -319,7 +356,7 @@ wsr_status sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch
     /* Passes of `batch` tokens (at most 8 when the table holds q4 matrices); the last tokens go in
        passes of the largest power of two that fits. */
     for (int32_t i = 0; i < n && batch > 8; ++i)
-        if (mats[i].fmt == WSR_Q4) batch = 8;
+        if (mats[i].fmt == WSR_Q4 || mats[i].fmt == WSR_I8) batch = 8;
     for (int32_t t = 0; t < n_tokens;) {
         int32_t T = batch;
         while (T > n_tokens - t) T >>= 1;

@@ -589,6 +589,124 @@ __device__ __forceinline__ void rows_q4_cols(const DevMat& d, int64_t r0, int64_
     for (; i < r1; ++i) q4_group_cols<1, T>(Wq, S, x, xcs, y, ycs, d.nc, i, lane);
 }
 
+/* ---- int8 rows with fp16 row scales -------------------------------------------------------------
+
+   The paper's protocol format (Sec. 3.1): w[i,k] = q[i,k] * s[i], q two's-complement int8, one fp16
+   scale per row.  A 16-byte chunk holds 16 codes; lane l takes chunks l, l + 64, ... of each row.
+   Decode: with u = q + 128 (the code XOR 0x80), masking a code word with 0x00FF00FF gives two exact
+   fp16 subnormals u * 2^-24 (codes 0 and 2 of the word) and the same after a shift by 8 gives codes
+   1 and 3; XOR and AND fuse into one three-input bit operation, so a word of 4 codes costs two bit
+   operations, one shift and two packed dot products.  Per chunk the products sum to
+   2^-24 (sum q x + 128 X), X the chunk's activation sum; the offset 2^-24 * 128 X depends on the
+   activations only and is formed once per chunk and shared by the rows.  The row total is scaled by
+   2^24 (exact) and then by the row scale, so a unit activation vector gives y = q * s exactly. */
+constexpr uint32_t I8_SIGN = 0x80808080u, I8_LOHALF = 0x00FF00FFu;
+constexpr uint32_t F16_I8_OFS = 0x00800080u;       /* 128 * 2^-24 in both halves (fp16 subnormal) */
+
+/* Activation pairs of one chunk in the order the decode produces codes: for code word d,
+   p[2d] = (x[4d], x[4d+2]), p[2d+1] = (x[4d+1], x[4d+3]); plus the chunk's offset term. */
+struct I8X {
+    uint32_t p[8];
+    float off;
+};
+
+__device__ __forceinline__ void i8_prep(u32x4 x0, u32x4 x1, I8X& q) {
+    const uint32_t X[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+    float off = 0.f;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+        q.p[2 * d + 0] = __builtin_amdgcn_perm(X[2 * d + 1], X[2 * d], 0x05040100u);
+        q.p[2 * d + 1] = __builtin_amdgcn_perm(X[2 * d + 1], X[2 * d], 0x07060302u);
+        off = dot2<FMT_F16>(F16_I8_OFS, q.p[2 * d + 0], off);
+        off = dot2<FMT_F16>(F16_I8_OFS, q.p[2 * d + 1], off);
+    }
+    q.off = off;
+}
+
+/* sum_k q x over one chunk, in units of 2^-24. */
+__device__ __forceinline__ float i8_chunk_dot(u32x4 w, const I8X& q) {
+    const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+    float t = 0.f;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+        t = dot2<FMT_F16>((wd[d] ^ I8_SIGN) & I8_LOHALF, q.p[2 * d + 0], t);
+        t = dot2<FMT_F16>((wd[d] >> 8 ^ 0x00800080u) & I8_LOHALF, q.p[2 * d + 1], t);
+    }
+    return t - q.off;
+}
+
+/* Rows [i, i + R) of an int8 matrix against T activation columns (T = 1: a single GEMV) in one
+   pass over the codes.  Column t of x starts xcs 16-byte chunks after column 0 (two chunks of x
+   per chunk of codes), its outputs ycs floats after.  Every (row, column) sum follows the same
+   chunk sequence and reduction tree whatever R, U and T are, so results do not depend on them. */
+template <int R, int U, int T>
+__device__ __forceinline__ void group_i8(g_u32x4* Wq, const uint16_t* S, g_u32x4* x, int64_t xcs, g_f32* y,
+                                         int64_t ycs, int64_t nc, int64_t i, int lane) {
+    constexpr int STEP = WAVE * U;
+    constexpr int N = R * T;
+    float acc[N];                                   /* entry t * R + r */
+#pragma unroll
+    for (int e = 0; e < N; ++e) acc[e] = 0.f;
+    g_u32x4* wr[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) wr[r] = Wq + (i + r) * nc;
+    for (int64_t c0 = 0; c0 < nc; c0 += STEP) {
+        u32x4 xv[T][U][2], wv[R][U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t c = c0 + u * WAVE + lane;
+            const bool ok = c < nc;
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+                xv[t][u][0] = ok ? load_reused(x + t * xcs + 2 * c) : zero4();
+                xv[t][u][1] = ok ? load_reused(x + t * xcs + 2 * c + 1) : zero4();
+            }
+#pragma unroll
+            for (int r = 0; r < R; ++r) wv[r][u] = ok ? load_once(wr[r] + c) : zero4();
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+                I8X q;
+                i8_prep(xv[t][u][0], xv[t][u][1], q);
+#pragma unroll
+                for (int r = 0; r < R; ++r) acc[t * R + r] += i8_chunk_dot(wv[r][u], q);
+            }
+    }
+    wave_sum_entries<N>(acc, lane);
+    auto out = [&](int e, float v) {
+        const float rs = f16_bits_to_f32(S[i + e % R]);
+        y[(e / R) * ycs + i + e % R] = v * 16777216.0f * rs;   /* 2^24 exact, then the row scale */
+    };
+    if constexpr (N <= WAVE) {
+        if ((lane & (WAVE / N - 1)) == 0) out(lane / (WAVE / N), acc[0]);
+    } else {
+#pragma unroll
+        for (int j = 0; j < N / WAVE; ++j) out(lane * (N / WAVE) + j, acc[j]);
+    }
+}
+
+/* Rows per wave and chunks per lane per step of the int8 loops for T columns (T <= 8). */
+template <int T> struct ColsI8 { static constexpr int R = 4, U = 4; };
+template <> struct ColsI8<2> { static constexpr int R = 4, U = 2; };
+template <> struct ColsI8<4> { static constexpr int R = 8, U = 1; };
+template <> struct ColsI8<8> { static constexpr int R = 8, U = 1; };
+
+/* Rows [r0, r1) of an int8 matrix for tokens token0 .. token0 + T - 1 in one pass over the codes. */
+template <int T, int R = ColsI8<T>::R, int U = ColsI8<T>::U>
+__device__ __forceinline__ void rows_i8(const DevMat& d, int64_t r0, int64_t r1, int32_t token0, int lane) {
+    static_assert(T <= 8, "int8 takes at most 8 columns per pass");
+    g_u32x4* Wq = as_global<g_u32x4*>(d.w);
+    const uint16_t* S = static_cast<const uint16_t*>(d.s);
+    g_u32x4* x = as_global<g_u32x4*>(static_cast<const char*>(d.x) + token0 * d.x_stride);
+    g_f32* y = as_global<g_f32*>(reinterpret_cast<char*>(d.y) + token0 * d.y_stride);
+    const int64_t xcs = d.x_stride / 16, ycs = d.y_stride / 4;
+    int64_t i = r0;
+    for (; i + R <= r1; i += R) group_i8<R, U, T>(Wq, S, x, xcs, y, ycs, d.nc, i, lane);
+    for (; i < r1; ++i) group_i8<1, U, T>(Wq, S, x, xcs, y, ycs, d.nc, i, lane);
+}
+
 /* Rows [r0, r1) of a q4 matrix.  With NB >= 2, when rows hold whole steps (nb a multiple of 64 U),
    the units (group of R rows, step) run as one software pipeline over NB register sets: the loads
    of the NB - 1 units after the current one are in flight while it is decoded.  The main loop is
@@ -684,7 +802,9 @@ __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, con
         /* A byte boundary maps to the first row group starting at or after it, the same way for
            the ranges on both sides, so the ranges still cover each row once and break only
            between whole groups of R rows. */
-        const int64_t g = fmt == FMT_Q4 ? (T == 1 ? RQ : RQC) : (T == 1 ? R16 : RC);
+        const int64_t g = fmt == FMT_Q4 ? (T == 1 ? RQ : RQC)
+                        : fmt == FMT_I8 ? ColsI8<(T <= 8 ? T : 8)>::R
+                                        : (T == 1 ? R16 : RC);
         const int64_t r0 = lo > d.cost0 ? ceil_div(lo - d.cost0, d.row_bytes * g) * g : 0;
         const int64_t e1 = ceil_div(hi - d.cost0, d.row_bytes * g) * g;
         const int64_t r1 = d.M < e1 ? d.M : e1;
@@ -696,6 +816,8 @@ __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, con
                 rows16<FMT_BF16, R16, U16>(d, r0, r1, token, lane);
             else if ((FMT == 0 || FMT == FMT_Q4) && fmt == FMT_Q4)
                 rows_q4<RQ, UQ, QNB>(d, r0, r1, token, lane);
+            else if ((FMT == 0 || FMT == FMT_I8) && fmt == FMT_I8)
+                rows_i8<1>(d, r0, r1, token, lane);
         } else {                                        /* tokens token .. token + T - 1 together */
             if ((FMT == 0 || FMT == FMT_F16) && fmt == FMT_F16)
                 rows16_cols<FMT_F16, T, RC, UC>(d, r0, r1, token, lane);
@@ -703,6 +825,7 @@ __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, con
                 rows16_cols<FMT_BF16, T, RC, UC>(d, r0, r1, token, lane);
             else if constexpr (T <= 8) {
                 if ((FMT == 0 || FMT == FMT_Q4) && fmt == FMT_Q4) rows_q4_cols<T, RQC>(d, r0, r1, token, lane);
+                else if ((FMT == 0 || FMT == FMT_I8) && fmt == FMT_I8) rows_i8<T>(d, r0, r1, token, lane);
             }
         }
     }

@@ -12,7 +12,7 @@
 
 namespace wsr {
 
-enum : int32_t { FMT_F16 = 1, FMT_BF16 = 2, FMT_Q4 = 3 };
+enum : int32_t { FMT_F16 = 1, FMT_BF16 = 2, FMT_Q4 = 3, FMT_I8 = 4 };
 
 struct alignas(16) DevMat {
     const void* w;          /* 16-bit weights or packed int4 codes                         */
@@ -35,14 +35,15 @@ hipError_t launch_probe(const float* buf, int64_t n, double* sum_dev, void* ws, 
 int64_t probe_grid(int64_t n);
 
 hipError_t launch_gemv(const DevMat& m, hipStream_t s);
-/* T activation columns per weight read (1, 2, 4, 8 or 16 for 16-bit formats, up to 8 for q4).
+/* T activation columns per weight read (1, 2, 4, 8 or 16 for 16-bit formats, up to 8 for q4 and
+   int8).
    m.x_stride and m.y_stride are the column strides in bytes. */
 hipError_t launch_gemv_cols(const DevMat& m, int T, hipStream_t s);
 /* Writes the table and clears the two tile counters at ctr (ctr may be null). */
 hipError_t launch_put_table(DevMat* dst, int64_t* cost, const DevMat* src, int n, unsigned* ctr,
                             hipStream_t s);
 /* One pass over the table's weights for tokens token .. token + T - 1 (T = 1, 2, 4, 8, 16; at most
-   8 when the table holds a q4 matrix). */
+   8 when the table holds a q4 or int8 matrix). */
 hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, int nmat, int64_t total_bytes,
                         int fmt_all, int32_t token, int T, unsigned* ctr, hipStream_t s);
 

@@ -177,10 +177,31 @@ __global__ __launch_bounds__(BLOCK) void k_gemv_q4_cols(DevMat d) {
     rows_q4_cols<T>(d, r0, std::min<int64_t>(r0 + R, d.M), 0, lane);
 }
 
+template <int T>
+__global__ __launch_bounds__(BLOCK) void k_gemv_i8(DevMat d) {
+    constexpr int R = ColsI8<T>::R;
+    const int lane = threadIdx.x & (WAVE - 1);
+    const int64_t wave = (int64_t)blockIdx.x * WAVES_PER_BLOCK + wave_in_block();
+    const int64_t r0 = wave * R;
+    if (r0 >= d.M) return;
+    rows_i8<T>(d, r0, std::min<int64_t>(r0 + R, d.M), 0, lane);
+}
+
+static hipError_t launch_gemv_i8(const DevMat& m, int T, hipStream_t s) {
+    switch (T) {
+        case 1: return launch_rows(k_gemv_i8<1>, m, ColsI8<1>::R, s);
+        case 2: return launch_rows(k_gemv_i8<2>, m, ColsI8<2>::R, s);
+        case 4: return launch_rows(k_gemv_i8<4>, m, ColsI8<4>::R, s);
+        case 8: return launch_rows(k_gemv_i8<8>, m, ColsI8<8>::R, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
 hipError_t launch_gemv_cols(const DevMat& m, int T, hipStream_t s) {
     if (m.M == 0) return hipSuccess;
     if (m.fmt == FMT_F16) return launch_gemv16_cols<FMT_F16>(m, T, s);
     if (m.fmt == FMT_BF16) return launch_gemv16_cols<FMT_BF16>(m, T, s);
+    if (m.fmt == FMT_I8) return launch_gemv_i8(m, T, s);
     if (m.fmt == FMT_Q4) {
         switch (T) {
             case 1: return launch_rows(k_gemv_q4_cols<1>, m, Cols4<1>::R, s);
@@ -203,6 +224,8 @@ hipError_t launch_gemv(const DevMat& m, hipStream_t s) {
         case FMT_Q4:
             return m.nc >= 256 ? launch_rows(k_gemv_q4<2, 2>, m, 2, s)
                                : launch_rows(k_gemv_q4<4, 1>, m, 4, s);
+        case FMT_I8:
+            return launch_gemv_i8(m, 1, s);
         default:
             return hipErrorInvalidValue;
     }
@@ -373,9 +396,12 @@ hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, int nmat, int64_
     const dim3 grid((unsigned)(cu_count() * SWEEP_BLOCKS_PER_CU_16));
     const int64_t tile = sweep_tile(total, (int64_t)grid.x * WAVES_PER_BLOCK);
     switch (fmt_all) {
+        case FMT_I8:
+            if (T > 8) return hipErrorInvalidValue;
+            return launch_sweep_cols<FMT_I8>(grid, T, s, tab, cost, nmat, total, tile, token, ctr);
         case FMT_F16: return launch_sweep_cols<FMT_F16>(grid, T, s, tab, cost, nmat, total, tile, token, ctr);
         case FMT_BF16: return launch_sweep_cols<FMT_BF16>(grid, T, s, tab, cost, nmat, total, tile, token, ctr);
-        default:   /* mixed formats; a table holding q4 comes with T <= 8 */
+        default:   /* mixed formats; a table holding q4 or int8 comes with T <= 8 */
             return launch_sweep_cols<0>(grid, T, s, tab, cost, nmat, total, tile, token, ctr);
     }
 }

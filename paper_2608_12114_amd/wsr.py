@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(_HERE, "libwsr.so")
 WSR_OK, WSR_E_ARG, WSR_E_ALIGN, WSR_E_SIZE, WSR_E_UNSUPPORTED, WSR_E_STATE, WSR_E_HIP = range(7)
 STATUS_NAMES = {0: "WSR_OK", 1: "WSR_E_ARG", 2: "WSR_E_ALIGN", 3: "WSR_E_SIZE",
                 4: "WSR_E_UNSUPPORTED", 5: "WSR_E_STATE", 6: "WSR_E_HIP"}
-WSR_F16, WSR_BF16, WSR_Q4 = 1, 2, 3
+WSR_F16, WSR_BF16, WSR_Q4, WSR_I8 = 1, 2, 3, 4
 WSR_REG_READONLY, WSR_REG_PIN, WSR_REG_PREPINNED = 1, 2, 4
 WSR_MAT_AFTER_PREVIOUS = 1
 
@@ -63,9 +63,11 @@ _L.wsr_decode_sweep.argtypes = [ctypes.POINTER(wsr_mat), _i32, _i32, _vp, _sz, _
 _L.wsr_gemv_f16_cols.argtypes = [_vp, _vp, _i64, _vp, _i64, _i64, _i64, _i32, ctypes.c_int, _vp]
 _L.wsr_decode_sweep_batched.argtypes = [ctypes.POINTER(wsr_mat), _i32, _i32, _i32, _vp, _sz, _vp]
 _L.wsr_gemv_q4_cols.argtypes = [_vp, _vp, _vp, _i64, _vp, _i64, _i64, _i64, _i32, _vp]
+_L.wsr_gemv_i8.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _vp]
+_L.wsr_gemv_i8_cols.argtypes = [_vp, _vp, _vp, _i64, _vp, _i64, _i64, _i64, _i32, _vp]
 for _f in ("wsr_register_host", "wsr_unregister_host", "wsr_probe_read", "wsr_gemv_f16",
            "wsr_gemv_q4", "wsr_decode_sweep", "wsr_gemv_f16_cols", "wsr_decode_sweep_batched",
-           "wsr_gemv_q4_cols"):
+           "wsr_gemv_q4_cols", "wsr_gemv_i8", "wsr_gemv_i8_cols"):
     getattr(_L, _f).restype = ctypes.c_int
 
 
@@ -139,6 +141,16 @@ def wsr_gemv_q4_cols(Wq, scales, x, x_col_stride: int, y, y_col_stride: int, M: 
 
 def wsr_gemv_q4(Wq, scales, x, y, M: int, K: int, stream=None) -> None:
     _check(_L.wsr_gemv_q4(_ptr(Wq), _ptr(scales), _ptr(x), _ptr(y), M, K, _stream(stream)))
+
+
+def wsr_gemv_i8(Wq, scales, x, y, M: int, K: int, stream=None) -> None:
+    _check(_L.wsr_gemv_i8(_ptr(Wq), _ptr(scales), _ptr(x), _ptr(y), M, K, _stream(stream)))
+
+
+def wsr_gemv_i8_cols(Wq, scales, x, x_col_stride: int, y, y_col_stride: int, M: int, K: int, T: int,
+                     stream=None) -> None:
+    _check(_L.wsr_gemv_i8_cols(_ptr(Wq), _ptr(scales), _ptr(x), x_col_stride, _ptr(y), y_col_stride, M, K, T,
+                               _stream(stream)))
 
 
 def make_mats(specs) -> ctypes.Array:

@@ -15,7 +15,7 @@ from __future__ import annotations
 from dataclasses import dataclass, field
 
 # storage formats of a weight matrix
-F16, BF16, Q4, INT8_ROWSCALE = "f16", "bf16", "q4", "int8_rowscale"
+F16, BF16, Q4, I8 = "f16", "bf16", "q4", "i8"      # i8: int8 codes with one fp16 scale per row
 
 # Distribution parameters of the synthetic inputs.
 W_SIGMA = 0.02          # 16-bit weights ~ N(0, 0.02), 0.02 the standard deviation
@@ -89,7 +89,7 @@ def matrix_bytes(M: int, K: int, fmt: str) -> int:
     if fmt == Q4:
         assert K % Q4_BLOCK == 0
         return M * K // 2 + M * (K // Q4_BLOCK) * 2
-    if fmt == INT8_ROWSCALE:
+    if fmt == I8:
         return M * K + M * 2
     raise ValueError(fmt)
 
@@ -102,7 +102,7 @@ def bytes_per_token(m: ModelShape, fmt: str, extra_vectors: int = 0) -> int:
 
 
 def embedding_bytes(m: ModelShape, fmt: str) -> int:
-    per = {F16: 2, BF16: 2, Q4: 0.5625, INT8_ROWSCALE: 1}[fmt]
+    per = {F16: 2, BF16: 2, Q4: 0.5625, I8: 1}[fmt]
     return int(m.vocab * m.d * per)
 
 
@@ -142,3 +142,12 @@ class SweepSpec:
 
 LLAMA8B_Q4 = ("llama3-8b-q4", LLAMA3_8B, Q4)
 LLAMA70B_BF16 = ("llama-70b-bf16", LLAMA_70B, BF16)
+
+# The matched protocol of Sec. 3.1 (Table 2): a single-token int8 GEMV with fp16 row scales over a
+# 12288 x 7168 matrix (88.1 MB with its scales), a pass visiting 12 such matrices.  Each matrix has
+# its own weights and its own activation vector.
+PROTOCOL_M, PROTOCOL_K, PROTOCOL_MATRICES = 12288, 7168, 12
+
+
+def protocol_matrices(n: int = PROTOCOL_MATRICES, M: int = PROTOCOL_M, K: int = PROTOCOL_K) -> list[Mat]:
+    return [Mat(i, f"w{i}", i, M, K, "attn") for i in range(n)]

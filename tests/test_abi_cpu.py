@@ -21,7 +21,7 @@ def declared():
 
 def test_exports_every_declared_symbol():
     names = declared()
-    assert len(names) == 13, names
+    assert len(names) == 15, names
     for n in names:
         assert hasattr(L, n), n
 
@@ -61,6 +61,13 @@ def test_gemv_argument_checks():
     assert _status(g, A, A, A, A, 4, 48, None) == wsr.WSR_E_ALIGN           # K % 32
     assert _status(g, A, A + 1, A, A, 4, 64, None) == wsr.WSR_E_ALIGN       # scales 2-byte
     assert _status(g, A, A, A, A, 0, 64, None) == wsr.WSR_OK
+    h = "wsr_gemv_i8"
+    assert _status(h, A, None, A, A, 4, 64, None) == wsr.WSR_E_ARG          # no row scales
+    assert _status(h, A, A, A, A, 4, 24, None) == wsr.WSR_E_ALIGN           # K % 16
+    assert _status(h, A + 8, A, A, A, 4, 64, None) == wsr.WSR_E_ALIGN       # codes 16-byte
+    assert _status(h, A, A + 1, A, A, 4, 64, None) == wsr.WSR_E_ALIGN       # scales 2-byte
+    assert _status(h, A, A, A, A, 0, 16, None) == wsr.WSR_OK
+    assert _status(f, A, A, A, 4, 16, wsr.WSR_I8, None) == wsr.WSR_E_ARG    # int8 is not 16-bit
 
 
 def test_probe_argument_checks():
@@ -102,6 +109,17 @@ def test_gemv_q4_cols_argument_checks():
     assert _status(f, None, None, None, 0, None, 0, 0, 64, 8, None) == wsr.WSR_OK   # M = 0
 
 
+def test_gemv_i8_cols_argument_checks():
+    f = "wsr_gemv_i8_cols"
+    for T in (0, 3, 16, -4):
+        assert _status(f, A, A, A, 64, A, 64, 4, 64, T, None) == wsr.WSR_E_ARG, T
+    assert _status(f, A, None, A, 64, A, 64, 4, 64, 2, None) == wsr.WSR_E_ARG
+    assert _status(f, A, A, A, 64, A, 64, 4, 40, 2, None) == wsr.WSR_E_ALIGN        # K % 16
+    assert _status(f, A, A, A, 72, A, 64, 4, 64, 2, None) == wsr.WSR_E_ALIGN        # x stride % 16
+    assert _status(f, A, A, A, 64, A, 8, 4, 64, 2, None) == wsr.WSR_E_ARG           # output columns overlap
+    assert _status(f, None, None, None, 0, None, 0, 0, 16, 8, None) == wsr.WSR_OK
+
+
 def test_batched_sweep_argument_checks():
     good = dict(fmt=2, M=8, K=64, w=A, x=A, y=A, x_tok_stride=128, y_tok_stride=32)
     mats = wsr.make_mats([good, good])
@@ -111,6 +129,8 @@ def test_batched_sweep_argument_checks():
         assert _status(f, mats, 2, 4, b, A, ws, None) == wsr.WSR_E_ARG, b
     q = wsr.make_mats([good, dict(good, fmt=3, scales=A, y_tok_stride=16)])
     assert _status(f, q, 2, 4, 16, A, ws, None) == wsr.WSR_E_ARG                  # q4 outputs overlap too
+    i8 = wsr.make_mats([good, dict(good, fmt=4, scales=A, y_tok_stride=16)])
+    assert _status(f, i8, 2, 4, 8, A, ws, None) == wsr.WSR_E_ARG                  # and int8 outputs
     shared = wsr.make_mats([good, dict(good, y_tok_stride=0)])
     assert _status(f, shared, 2, 4, 2, A, ws, None) == wsr.WSR_E_ARG               # tokens would share y
     assert _status(f, mats, 2, 0, 2, A, ws, None) == wsr.WSR_E_ARG                 # n_tokens < 1
@@ -129,6 +149,7 @@ def test_sweep_argument_checks():
     assert _status(f, mats, 0, 1, None, 0, None) == wsr.WSR_OK              # empty sweep
     for bad, st in ((dict(good, fmt=9), wsr.WSR_E_ARG), (dict(good, flags=2), wsr.WSR_E_ARG),
                     (dict(good, K=60), wsr.WSR_E_ALIGN), (dict(good, fmt=3), wsr.WSR_E_ARG),
+                    (dict(good, fmt=4), wsr.WSR_E_ARG), (dict(good, fmt=4, scales=A, K=40), wsr.WSR_E_ALIGN),
                     (dict(good, x_tok_stride=8), wsr.WSR_E_ALIGN),
                     (dict(good, y_tok_stride=-4), wsr.WSR_E_ALIGN),
                     (dict(good, x=A + 8), wsr.WSR_E_ALIGN)):

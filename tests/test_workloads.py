@@ -12,11 +12,11 @@ def test_qwen72b_bytes_per_token_matches_paper():
     m = wl.QWEN25_72B
     # the model also reads per-layer vectors: q/k/v biases and two norms per layer, one final norm
     vectors = (m.layers * (m.n_q * m.head_dim + 2 * m.n_kv * m.head_dim) + m.layers * 2 * m.d + m.d)
-    b = wl.bytes_per_token(m, wl.INT8_ROWSCALE) + vectors * 2
+    b = wl.bytes_per_token(m, wl.I8) + vectors * 2
     assert round(b / 1e9, g["decimals"]) == g["value"]
     # the matrices and scales alone are within 0.01 GB of it; the embedding table is excluded
-    assert abs(wl.bytes_per_token(m, wl.INT8_ROWSCALE) / 1e9 - g["value"]) < 0.01
-    assert (b + wl.embedding_bytes(m, wl.INT8_ROWSCALE)) / 1e9 > g["value"] + 1.0
+    assert abs(wl.bytes_per_token(m, wl.I8) / 1e9 - g["value"]) < 0.01
+    assert (b + wl.embedding_bytes(m, wl.I8)) / 1e9 > g["value"] + 1.0
     for tok_s, gbps in GOLD["qwen25_72b_logical_rates"]["pairs_tok_s_to_gbps"]:
         assert round(tok_s * g["value"]) == gbps
 
