@@ -687,11 +687,17 @@ __device__ __forceinline__ void group_i8(g_u32x4* Wq, const uint16_t* S, g_u32x4
     }
 }
 
-/* Rows per wave and chunks per lane per step of the int8 loops for T columns (T <= 8). */
-template <int T> struct ColsI8 { static constexpr int R = 4, U = 4; };
-template <> struct ColsI8<2> { static constexpr int R = 4, U = 2; };
-template <> struct ColsI8<4> { static constexpr int R = 8, U = 1; };
-template <> struct ColsI8<8> { static constexpr int R = 8, U = 1; };
+/* Rows per wave and chunks per lane per step of the int8 sweep loops for T columns (T <= 8): eight
+   rows share each activation chunk's preparation, one chunk per lane per step keeps the register
+   count low enough for several waves per SIMD. */
+template <int T> struct ColsI8 { static constexpr int R = 8, U = 1; };
+/* The same for the standalone int8 GEMV kernels (one group of R rows per wave). */
+template <int T> struct GemvI8 { static constexpr int R = 4, U = 4; };
+template <> struct GemvI8<2> { static constexpr int R = 4, U = 2; };
+template <> struct GemvI8<4> { static constexpr int R = 8, U = 1; };
+template <> struct GemvI8<8> { static constexpr int R = 8, U = 1; };
+/* Register sets in flight in the single-column int8 row loop. */
+constexpr int I8_NB = 3;
 
 /* Rows [r0, r1) of an int8 matrix for tokens token0 .. token0 + T - 1 in one pass over the codes. */
 template <int T, int R = ColsI8<T>::R, int U = ColsI8<T>::U>
@@ -705,6 +711,94 @@ __device__ __forceinline__ void rows_i8(const DevMat& d, int64_t r0, int64_t r1,
     int64_t i = r0;
     for (; i + R <= r1; i += R) group_i8<R, U, T>(Wq, S, x, xcs, y, ycs, d.nc, i, lane);
     for (; i < r1; ++i) group_i8<1, U, T>(Wq, S, x, xcs, y, ycs, d.nc, i, lane);
+}
+
+/* One step of the int8 row loop: R rows x U chunks of codes and the U activation chunk pairs. */
+template <int R, int U>
+struct I8Step {
+    u32x4 w[R][U];
+    u32x4 x[U][2];
+};
+
+/* Rows [r0, r1) of an int8 matrix, one column, with NB register sets in flight: while one unit
+   (group of R rows, step) is decoded the loads of the next NB - 1 units are outstanding, across
+   row-group boundaries, as in the q4 loop below.  Needs rows made of whole steps (nc a multiple of
+   64 U); otherwise, and for the rows left over, group_i8 runs.  Every sum takes the chunks and
+   the reduction tree of group_i8, so the results are those of rows_i8<1>. */
+template <int R, int U, int NB>
+__device__ __forceinline__ void rows_i8_pipe(const DevMat& d, int64_t r0, int64_t r1, int32_t token, int lane) {
+    g_u32x4* Wq = as_global<g_u32x4*>(d.w);
+    const uint16_t* S = static_cast<const uint16_t*>(d.s);
+    g_u32x4* x = as_global<g_u32x4*>(static_cast<const char*>(d.x) + token * d.x_stride);
+    g_f32* y = as_global<g_f32*>(reinterpret_cast<char*>(d.y) + token * d.y_stride);
+    const int64_t nc = d.nc;
+    constexpr int STEP = WAVE * U;
+    const int64_t ngroups = (r1 - r0) / R;
+    int64_t i = r0;
+    if (ngroups > 0 && nc > 0 && nc % STEP == 0) {
+        const int64_t steps = nc / STEP;                 /* steps per row group */
+        const int64_t n = ngroups * steps;               /* units */
+        float acc[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) acc[r] = 0.f;
+        int64_t gl = 0, kl = 0;                          /* next unit to load   */
+        int64_t gc = 0, kc = 0;                          /* next unit to decode */
+        auto load = [&](I8Step<R, U>& st) {
+            const int64_t i0 = r0 + gl * R;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t c = kl * STEP + u * WAVE + lane;
+                st.x[u][0] = load_reused(x + 2 * c);
+                st.x[u][1] = load_reused(x + 2 * c + 1);
+#pragma unroll
+                for (int r = 0; r < R; ++r) st.w[r][u] = load_once(Wq + (i0 + r) * nc + c);
+            }
+            if (++kl == steps) { kl = 0; ++gl; }
+        };
+        auto decode = [&](const I8Step<R, U>& st) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                I8X q;
+                i8_prep(st.x[u][0], st.x[u][1], q);
+#pragma unroll
+                for (int r = 0; r < R; ++r) acc[r] += i8_chunk_dot(st.w[r][u], q);
+            }
+            if (kc + 1 == steps) {
+                const int64_t i0 = r0 + gc * R;
+                wave_sum_entries<R>(acc, lane);
+                if ((lane & (WAVE / R - 1)) == 0) {
+                    const int e = lane / (WAVE / R);
+                    y[i0 + e] = acc[0] * 16777216.0f * f16_bits_to_f32(S[i0 + e]);
+                }
+#pragma unroll
+                for (int r = 0; r < R; ++r) acc[r] = 0.f;
+            }
+            if (++kc == steps) { kc = 0; ++gc; }
+        };
+        I8Step<R, U> buf[NB];
+#pragma unroll
+        for (int j = 0; j < NB - 1; ++j)
+            if (j < n) load(buf[j]);
+        int64_t u = 0;                                   /* buf[j] holds unit u + j, j < NB - 1 */
+        for (; u + 2 * NB - 1 <= n; u += NB) {
+#pragma unroll
+            for (int j = 0; j < NB; ++j) {
+                load(buf[(j + NB - 1) % NB]);            /* unit u + j + NB - 1 */
+                __builtin_amdgcn_sched_barrier(0);       /* keep those loads ahead of the decode */
+                decode(buf[j]);                          /* unit u + j */
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 2 * NB - 1; ++j) {
+            if (u + j < n) {
+                if (u + j + NB - 1 < n) load(buf[(j + NB - 1) % NB]);
+                decode(buf[j % NB]);
+            }
+        }
+        i = r0 + ngroups * R;
+    }
+    for (; i + R <= r1; i += R) group_i8<R, U, 1>(Wq, S, x, 0, y, 0, nc, i, lane);
+    for (; i < r1; ++i) group_i8<1, U, 1>(Wq, S, x, 0, y, 0, nc, i, lane);
 }
 
 /* Rows [r0, r1) of a q4 matrix.  With NB >= 2, when rows hold whole steps (nb a multiple of 64 U),
@@ -817,7 +911,7 @@ __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, con
             else if ((FMT == 0 || FMT == FMT_Q4) && fmt == FMT_Q4)
                 rows_q4<RQ, UQ, QNB>(d, r0, r1, token, lane);
             else if ((FMT == 0 || FMT == FMT_I8) && fmt == FMT_I8)
-                rows_i8<1>(d, r0, r1, token, lane);
+                rows_i8_pipe<ColsI8<1>::R, ColsI8<1>::U, I8_NB>(d, r0, r1, token, lane);
         } else {                                        /* tokens token .. token + T - 1 together */
             if ((FMT == 0 || FMT == FMT_F16) && fmt == FMT_F16)
                 rows16_cols<FMT_F16, T, RC, UC>(d, r0, r1, token, lane);

@@ -15,12 +15,12 @@ namespace wsr {
 enum : int32_t { FMT_F16 = 1, FMT_BF16 = 2, FMT_Q4 = 3, FMT_I8 = 4 };
 
 struct alignas(16) DevMat {
-    const void* w;          /* 16-bit weights or packed int4 codes                         */
-    const void* s;          /* q4 block scales                                              */
+    const void* w;          /* 16-bit weights, packed int4 codes or int8 codes              */
+    const void* s;          /* q4 block scales or int8 row scales                           */
     const void* x;          /* activation of token 0                                        */
     float* y;               /* output of token 0                                            */
     int64_t M;              /* rows                                                         */
-    int64_t nc;             /* per row: 16-byte weight chunks (16-bit) or 32-weight blocks  */
+    int64_t nc;             /* per row: 16-byte chunks (16-bit, int8) or 32-weight blocks    */
     int64_t x_stride;       /* bytes between tokens                                         */
     int64_t y_stride;
     int64_t cost0;          /* weight-stream byte offset of row 0 within its launch         */

@@ -179,20 +179,20 @@ __global__ __launch_bounds__(BLOCK) void k_gemv_q4_cols(DevMat d) {
 
 template <int T>
 __global__ __launch_bounds__(BLOCK) void k_gemv_i8(DevMat d) {
-    constexpr int R = ColsI8<T>::R;
+    constexpr int R = GemvI8<T>::R;
     const int lane = threadIdx.x & (WAVE - 1);
     const int64_t wave = (int64_t)blockIdx.x * WAVES_PER_BLOCK + wave_in_block();
     const int64_t r0 = wave * R;
     if (r0 >= d.M) return;
-    rows_i8<T>(d, r0, std::min<int64_t>(r0 + R, d.M), 0, lane);
+    rows_i8<T, R, GemvI8<T>::U>(d, r0, std::min<int64_t>(r0 + R, d.M), 0, lane);
 }
 
 static hipError_t launch_gemv_i8(const DevMat& m, int T, hipStream_t s) {
     switch (T) {
-        case 1: return launch_rows(k_gemv_i8<1>, m, ColsI8<1>::R, s);
-        case 2: return launch_rows(k_gemv_i8<2>, m, ColsI8<2>::R, s);
-        case 4: return launch_rows(k_gemv_i8<4>, m, ColsI8<4>::R, s);
-        case 8: return launch_rows(k_gemv_i8<8>, m, ColsI8<8>::R, s);
+        case 1: return launch_rows(k_gemv_i8<1>, m, GemvI8<1>::R, s);
+        case 2: return launch_rows(k_gemv_i8<2>, m, GemvI8<2>::R, s);
+        case 4: return launch_rows(k_gemv_i8<4>, m, GemvI8<4>::R, s);
+        case 8: return launch_rows(k_gemv_i8<8>, m, GemvI8<8>::R, s);
         default: return hipErrorInvalidValue;
     }
 }
@@ -344,9 +344,47 @@ static int cu_count() {
 /* 16-bit weights: tiles, 4 rows x 4 KiB steps per wave, one block (4 waves) per CU (few, long
    streams).  q4: spans of about 64 KiB per wave, 8 rows x 1 block per lane per step (eight rows
    share each block's activation decode), two register sets in flight; the grid is sized so that
-   blocks retire and are replaced throughout the token (16,100 blocks for 4.2 GB). */
+   blocks retire and are replaced throughout the token (16,100 blocks for 4.2 GB).  int8: spans of
+   about SWEEP_SPAN_I8[T] bytes per wave with 8 rows x 1 chunk per lane per step and, for one
+   column, three register sets in flight; tiles with one block per CU reach about half the rate
+   (one wave per SIMD cannot cover the latency at each row group's start). */
 constexpr int SWEEP_BLOCKS_PER_CU_16 = 1;
 constexpr int64_t SWEEP_SPAN_Q4 = 64 << 10;
+constexpr int64_t SWEEP_SPAN_I8[4] = {32 << 10, 32 << 10, 128 << 10, 128 << 10};   /* T = 1, 2, 4, 8 */
+
+/* Grid of a span-scheduled sweep: about `span` bytes per wave, at least one wave per SIMD. */
+static hipError_t span_grid(int64_t total, int64_t span, dim3& g) {
+    const int64_t waves = std::max<int64_t>((int64_t)cu_count() * WAVES_PER_BLOCK, (total + span - 1) / span);
+    const int64_t blocks = (waves + WAVES_PER_BLOCK - 1) / WAVES_PER_BLOCK;
+    if (blocks > INT32_MAX) return hipErrorInvalidValue;
+    g = dim3((unsigned)blocks);
+    return hipSuccess;
+}
+
+template <int FMT, int T>
+static void launch_sweep_spans(dim3 g, hipStream_t s, const DevMat* tab, const int64_t* cost, int nmat,
+                               int64_t total, int32_t token) {
+    hipLaunchKernelGGL((k_sweep<FMT, SCHED_SPANS, 4, 4, 8, 1, 2, T>), g, dim3(BLOCK), 0, s, tab, cost, nmat, total,
+                       (int64_t)0, (int64_t)0, token, nullptr);
+}
+
+/* q4 and int8 sweeps (T <= 8) over spans. */
+template <int FMT>
+static hipError_t launch_sweep_quant(int T, hipStream_t s, const DevMat* tab, const int64_t* cost, int nmat,
+                                     int64_t total, int32_t token) {
+    const int ti = T == 1 ? 0 : T == 2 ? 1 : T == 4 ? 2 : 3;
+    dim3 g;
+    const hipError_t e = span_grid(total, FMT == FMT_Q4 ? SWEEP_SPAN_Q4 : SWEEP_SPAN_I8[ti], g);
+    if (e != hipSuccess) return e;
+    switch (T) {
+        case 1: launch_sweep_spans<FMT, 1>(g, s, tab, cost, nmat, total, token); break;
+        case 2: launch_sweep_spans<FMT, 2>(g, s, tab, cost, nmat, total, token); break;
+        case 4: launch_sweep_spans<FMT, 4>(g, s, tab, cost, nmat, total, token); break;
+        case 8: launch_sweep_spans<FMT, 8>(g, s, tab, cost, nmat, total, token); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
 
 /* 16-bit (or mixed-format) sweep over tiles, tokens token .. token + T - 1 per weight pass. */
 template <int FMT, int T>
@@ -373,32 +411,11 @@ static hipError_t launch_sweep_cols(dim3 grid, int T, hipStream_t s, const DevMa
 hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, int nmat, int64_t total, int fmt_all,
                         int32_t token, int T, unsigned* ctr, hipStream_t s) {
     if (nmat == 0 || total == 0) return hipSuccess;
-    if (fmt_all == FMT_Q4) {
-        /* About SWEEP_SPAN_Q4 bytes per wave, at least one wave per SIMD. */
-        const int64_t waves = std::max<int64_t>((int64_t)cu_count() * WAVES_PER_BLOCK,
-                                                (total + SWEEP_SPAN_Q4 - 1) / SWEEP_SPAN_Q4);
-        const int64_t blocks = (waves + WAVES_PER_BLOCK - 1) / WAVES_PER_BLOCK;
-        if (blocks > INT32_MAX) return hipErrorInvalidValue;
-        const dim3 g((unsigned)blocks);
-#define WSR_Q4_SWEEP(TT)                                                                                      \
-    hipLaunchKernelGGL((k_sweep<FMT_Q4, SCHED_SPANS, 4, 4, 8, 1, 2, TT>), g, dim3(BLOCK), 0, s, tab, cost, nmat, \
-                       total, (int64_t)0, (int64_t)0, token, ctr)
-        switch (T) {
-            case 1: WSR_Q4_SWEEP(1); break;
-            case 2: WSR_Q4_SWEEP(2); break;
-            case 4: WSR_Q4_SWEEP(4); break;
-            case 8: WSR_Q4_SWEEP(8); break;
-            default: return hipErrorInvalidValue;
-        }
-#undef WSR_Q4_SWEEP
-        return hipGetLastError();
-    }
+    if (fmt_all == FMT_Q4) return launch_sweep_quant<FMT_Q4>(T, s, tab, cost, nmat, total, token);
+    if (fmt_all == FMT_I8) return launch_sweep_quant<FMT_I8>(T, s, tab, cost, nmat, total, token);
     const dim3 grid((unsigned)(cu_count() * SWEEP_BLOCKS_PER_CU_16));
     const int64_t tile = sweep_tile(total, (int64_t)grid.x * WAVES_PER_BLOCK);
     switch (fmt_all) {
-        case FMT_I8:
-            if (T > 8) return hipErrorInvalidValue;
-            return launch_sweep_cols<FMT_I8>(grid, T, s, tab, cost, nmat, total, tile, token, ctr);
         case FMT_F16: return launch_sweep_cols<FMT_F16>(grid, T, s, tab, cost, nmat, total, tile, token, ctr);
         case FMT_BF16: return launch_sweep_cols<FMT_BF16>(grid, T, s, tab, cost, nmat, total, tile, token, ctr);
         default:   /* mixed formats; a table holding q4 or int8 comes with T <= 8 */
