@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define WSR_ABI_VERSION 2
+#define WSR_ABI_VERSION 3
 
 typedef enum {
     WSR_OK = 0,
@@ -195,6 +195,65 @@ wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, vo
    must have y_tok_stride >= 4 M.  ws as for wsr_decode_sweep. */
 wsr_status wsr_decode_sweep_batched(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch,
                                     void* ws, size_t ws_bytes, void* stream);
+
+/* ---- per-use copy endpoint (Sec. 8.1; Table 2, pipelined double-buffered copy; Sec. 7.2,
+   overlapped streaming) ---------------------------------------------------------------------
+
+   wsr_sweep_staged: the outputs of wsr_decode_sweep for the single token `token`, bit for bit,
+   with every matrix's weights (and scales) copied per use from wherever they live (pageable or
+   pinned host memory, or device memory) into a device staging buffer instead of being read in
+   place.  `stage` (device memory, 256-byte aligned) is split into two halves; each matrix goes in
+   chunks of whole rows that fit a half (codes first, scales after them at a 256-byte boundary),
+   alternating halves.  Copies run on `copy_stream` and GEMVs on `stream`: the copy of a chunk into
+   a half waits for the GEMV that last read that half, and each GEMV waits for its chunk's copy,
+   so the copy of chunk k + 1 overlaps the GEMV of chunk k.  The first copy waits for the work
+   already enqueued on `stream`; on return, all work of the call is ordered before later work on
+   `stream`.  Use distinct streams for overlap (the same stream also works, serially).  The source
+   memory must stay valid and unchanged until the copies have run.  A copy from pageable host
+   memory may run on the host as soon as it is issued, ahead of the stream's earlier waits; for such
+   sources the call therefore waits on the host, before each copy into a half, until the GEMV that
+   last read that half has run (the call blocks).  mats: as wsr_decode_sweep, except that w and scales may
+   be host pointers; x and y device memory.  WSR_E_SIZE if half of stage_bytes, less 256, holds no
+   row of some matrix.  Calls on one device are serialised while they enqueue (events shared per
+   device). */
+wsr_status wsr_sweep_staged(const wsr_mat* mats, int32_t n, int32_t token, void* stage, size_t stage_bytes,
+                            void* stream, void* copy_stream);
+
+/* ---- endpoint selection (Alg. 2, Sec. 8.1) -------------------------------------------------------
+
+   wsr_host_resident_pages: how many of the pages spanning [host, host + bytes) are resident in
+   memory (mincore), for Alg. 2's check that a prefaulted mapped set is resident and that it
+   survives one pass of every arm (page-cache residency control, Table 5).  WSR_E_ARG if part of
+   the range is not mapped. */
+wsr_status wsr_host_resident_pages(const void* host, size_t bytes, size_t* resident_pages, size_t* total_pages);
+
+/* wsr_select_endpoint: Alg. 2 over measured endpoint rates.  Path time is W / B per endpoint
+   (Sec. 8.1).  In order: a mapped set that is not resident stops with WSR_EP_STORAGE_BOUND; the
+   resident endpoint is dropped when resident_ok is 0 (its allocation failed, or the mapping was
+   evicted after one pass of every arm); endpoints named in `excluded` (bit 1 << WSR_EP_x: import
+   or capacity limits) or with rate <= 0 (not measured) are dropped; among the survivors the
+   fastest wins, except that mapping wins whenever its time exceeds the fastest by at most
+   theta (a fraction: 0.05 is the paper's 5 % band) of the fastest time.  *choice receives the
+   endpoint (WSR_EP_NONE if none survives); times_ms, if not NULL, receives W / B in milliseconds
+   for map, resident and copy (-1 where not measured). */
+typedef enum {
+    WSR_EP_NONE = 0,
+    WSR_EP_MAP = 1,             /* read the file pages (host memory) in place                    */
+    WSR_EP_RESIDENT = 2,        /* one copy into device memory, reused by every pass            */
+    WSR_EP_COPY = 3,            /* per-use copy (wsr_sweep_staged)                               */
+    WSR_EP_STORAGE_BOUND = 4    /* the mapped set is not resident: outside the studied regime   */
+} wsr_endpoint;
+
+typedef struct wsr_endpoint_probe {
+    double w_bytes;             /* working set W (bytes)                                          */
+    double rate[3];             /* B_map, B_resident, B_copy in bytes/s, measured with one kernel */
+    int32_t mapped_resident;    /* every page of the mapped set resident after prefaulting        */
+    int32_t resident_ok;        /* resident arm allocated and the mapping survived every arm     */
+    uint32_t excluded;          /* endpoints dropped for import or capacity limits               */
+    int32_t reserved;           /* 0                                                              */
+} wsr_endpoint_probe;
+
+wsr_status wsr_select_endpoint(const wsr_endpoint_probe* p, double theta, int32_t* choice, double* times_ms);
 
 #ifdef __cplusplus
 }

@@ -1,7 +1,9 @@
 """Build libwsr.so (HIP kernels for gfx950 plus the C ABI) in-tree with hipcc."""
 from __future__ import annotations
 
+import collections
 import os
+import re
 import subprocess
 
 PKG = os.path.dirname(os.path.abspath(__file__))
@@ -21,10 +23,38 @@ DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-p
           "-ffp-contract=fast", "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]
 
 
+# A toolchain hazard checked on every build.  The AMDGPU backend's pre-emit peephole deletes an
+# `s_and_b64 vcc, vcc, exec` after a vector compare when a VCC branch follows, without checking
+# whether a scalar select still reads the SCC that instruction defines; the select then takes a
+# stale condition.  It turned a row clamp min(r0 + R, M) into r0 + R, so a kernel read and wrote
+# rows past the end of its matrix.  The compile prints the machine code just before and after that
+# pass (printing does not change code generation), and the build fails if the pass removed any
+# instruction whose SCC definition was live.
+_PEEPHOLE = "si-pre-emit-peephole"
+_MIR_FLAGS = ["-mllvm", f"-print-before={_PEEPHOLE}", "-mllvm", f"-print-after={_PEEPHOLE}"]
+
+
+def dropped_live_scc(dump: str) -> list[str]:
+    """Instructions with a live SCC definition present before the pass and gone after it."""
+    parts = re.split(r"^# \*\*\* IR Dump (Before|After) [^\n]*\n", dump, flags=re.M)
+    seen: dict[str, dict[str, collections.Counter]] = {}
+    for kind, body in zip(parts[1::2], parts[2::2]):
+        m = re.search(r"^# Machine code for function (\S+?):", body, re.M)
+        if not m:
+            continue
+        live = collections.Counter(l.strip() for l in body.splitlines() if "implicit-def $scc" in l)
+        seen.setdefault(m.group(1), {})[kind] = live
+    out = []
+    for fn, d in seen.items():
+        for line, n in (d.get("Before", collections.Counter()) - d.get("After", collections.Counter())).items():
+            out.append(f"{fn}: {line} (x{n})")
+    return out
+
+
 def _run(cmd):
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
-        raise RuntimeError(f"build failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+        raise RuntimeError(f"build failed: {' '.join(cmd)}\n{r.stdout[-4000:]}\n{r.stderr[-4000:]}")
     return r
 
 
@@ -32,7 +62,13 @@ def build(verbose: bool = False) -> str:
     os.makedirs(OUT_DIR, exist_ok=True)
     k_obj = os.path.join(OUT_DIR, "wsr_kernels.o")
     a_obj = os.path.join(OUT_DIR, "wsr_api.o")
-    _run(["hipcc", *COMMON, *DEVICE, "-c", os.path.join(CSRC, "wsr_kernels.hip"), "-o", k_obj])
+    r = _run(["hipcc", *COMMON, *DEVICE, *_MIR_FLAGS, "-c", os.path.join(CSRC, "wsr_kernels.hip"), "-o", k_obj])
+    if "IR Dump Before" not in r.stderr:
+        raise RuntimeError("build: the compiler printed no machine code for the peephole check")
+    dropped = dropped_live_scc(r.stderr)
+    if dropped:
+        raise RuntimeError("build: the pre-emit peephole removed live SCC definitions (miscompiled "
+                           "selects):\n  " + "\n  ".join(dropped))
     _run(["hipcc", *COMMON, "-c", os.path.join(CSRC, "wsr_api.cpp"), "-o", a_obj])
     tmp = LIB_PATH + ".tmp"
     _run(["hipcc", "-shared", "-fPIC", f"--offload-arch={ARCH}", k_obj, a_obj, "-o", tmp])

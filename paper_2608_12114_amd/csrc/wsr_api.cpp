@@ -4,8 +4,10 @@
  * so a rejected call leaves the stream untouched.  Argument checks make no HIP call.
  */
 #include <hip/hip_runtime_api.h>
+#include <sys/mman.h>
 #include <unistd.h>
 
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <map>
@@ -381,6 +383,198 @@ wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, vo
 wsr_status wsr_decode_sweep_batched(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch,
                                     void* ws, size_t ws_bytes, void* stream) {
     return sweep(mats, n, n_tokens, batch, ws, ws_bytes, stream);
+}
+
+}  // extern "C"
+
+/* ---- per-use copy endpoint, residency query, endpoint selection ------------------------------ */
+
+namespace {
+
+/* Bytes per row of a matrix as the caller stores it: weights or codes, and scales. */
+void row_parts(int fmt, int64_t K, int64_t& code_row, int64_t& scale_row) {
+    if (fmt == WSR_Q4) {
+        code_row = K / 2;
+        scale_row = (K / 32) * 2;
+    } else if (fmt == WSR_I8) {
+        code_row = K;
+        scale_row = 2;
+    } else {
+        code_row = K * 2;
+        scale_row = 0;
+    }
+}
+
+int64_t pad256(int64_t v) { return (v + 255) / 256 * 256; }
+
+/* Events of the staged sweep, created once per device and kept for the life of the process; a
+   mutex per device serialises the enqueueing of calls that share them (a wait enqueued on an
+   event refers to the record made before it, so a later call may record the events again). */
+struct StageEvents {
+    std::mutex mu;
+    bool made = false;
+    hipEvent_t start{}, copied[2]{}, consumed[2]{};
+};
+StageEvents g_stage_ev[64];
+
+hipError_t stage_events(int dev, StageEvents*& out) {
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    StageEvents& e = g_stage_ev[dev];
+    out = &e;
+    if (e.made) return hipSuccess;
+    hipEvent_t* all[5] = {&e.start, &e.copied[0], &e.copied[1], &e.consumed[0], &e.consumed[1]};
+    for (hipEvent_t* p : all) {
+        const hipError_t r = hipEventCreateWithFlags(p, hipEventDisableTiming);
+        if (r != hipSuccess) return r;
+    }
+    e.made = true;
+    return hipSuccess;
+}
+
+/* True for host memory the runtime has not registered (pageable).  A copy from such memory may be
+   carried out on the host when it is issued, ahead of the waits already enqueued on its stream, so
+   the staged sweep orders those copies with host-side waits instead. */
+bool pageable(const void* p) {
+    if (!p) return false;
+    hipPointerAttribute_t a{};
+    if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+        (void)hipGetLastError();                   /* do not leave the error for a later check */
+        return true;
+    }
+    return a.type == hipMemoryTypeUnregistered;
+}
+
+}  // namespace
+
+extern "C" {
+
+wsr_status wsr_sweep_staged(const wsr_mat* mats, int32_t n, int32_t token, void* stage, size_t stage_bytes,
+                            void* stream, void* copy_stream) {
+    if (n < 0 || token < 0) return fail(WSR_E_ARG, "sweep_staged: n=%d token=%d", n, token);
+    if (n == 0) return ok();
+    if (!mats || !stage) return fail(WSR_E_ARG, "sweep_staged: null pointer");
+    if (!aligned(stage, 256)) return fail(WSR_E_ALIGN, "sweep_staged: staging buffer must be 256-byte aligned");
+    const int64_t half = (int64_t)(stage_bytes / 2) / 256 * 256;
+    char who[64];
+    for (int32_t i = 0; i < n; ++i) {
+        const wsr_mat& m = mats[i];
+        std::snprintf(who, sizeof who, "sweep_staged: matrix %d", i);
+        wsr_status st = check_matrix(m.fmt, m.M, m.K, m.w, m.scales, m.x, m.y, who);
+        if (st != WSR_OK) return st;
+        if (m.flags & ~WSR_MAT_AFTER_PREVIOUS) return fail(WSR_E_ARG, "%s: unknown flags %#x", who, m.flags);
+        if (m.x_tok_stride < 0 || m.y_tok_stride < 0 || m.x_tok_stride % 16 || m.y_tok_stride % 4)
+            return fail(WSR_E_ALIGN, "%s: token strides must be >= 0 and multiples of 16 (x) and 4 (y)", who);
+        if (!mul_fits(m.x_tok_stride, (int64_t)token + 1) || !mul_fits(m.y_tok_stride, (int64_t)token + 1))
+            return fail(WSR_E_SIZE, "%s: token strides overflow", who);
+        int64_t code_row, scale_row;
+        row_parts(m.fmt, m.K, code_row, scale_row);
+        if (m.M > 0 && code_row + scale_row > 0 && half < 256 + code_row + scale_row)
+            return fail(WSR_E_SIZE, "%s: half of the staging buffer (%lld bytes) holds no row of %lld bytes", who,
+                        (long long)half, (long long)(code_row + scale_row));
+    }
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "sweep_staged: device");
+    StageEvents* ev = nullptr;
+    e = stage_events(dev, ev);
+    if (e != hipSuccess) return hip_fail(e, "sweep_staged: events");
+    std::lock_guard<std::mutex> lock(ev->mu);
+    hipStream_t s = static_cast<hipStream_t>(stream), cs = static_cast<hipStream_t>(copy_stream);
+    char* buf[2] = {static_cast<char*>(stage), static_cast<char*>(stage) + half};
+    /* The first copy waits for the work already on `stream` (an earlier reader of the buffer). */
+    if ((e = hipEventRecord(ev->start, s)) != hipSuccess || (e = hipStreamWaitEvent(cs, ev->start, 0)) != hipSuccess)
+        return hip_fail(e, "sweep_staged: ordering");
+    int64_t k = 0;
+    bool started = false;                            /* the host has waited for `start` */
+    for (int32_t i = 0; i < n; ++i) {
+        const wsr_mat& m = mats[i];
+        if (m.M == 0) continue;
+        int64_t code_row, scale_row;
+        row_parts(m.fmt, m.K, code_row, scale_row);
+        const bool host_wait = pageable(m.w) || (scale_row > 0 && pageable(m.scales));
+        const int64_t per = code_row + scale_row > 0 ? (half - 256) / (code_row + scale_row) : m.M;
+        const char* x = static_cast<const char*>(m.x) + (int64_t)token * m.x_tok_stride;
+        char* y = reinterpret_cast<char*>(m.y) + (int64_t)token * m.y_tok_stride;
+        for (int64_t r0 = 0; r0 < m.M; r0 += per, ++k) {
+            const int64_t rows = std::min<int64_t>(per, m.M - r0);
+            const int b = (int)(k & 1);
+            const int64_t soff = pad256(rows * code_row);
+            /* Buffer b is free once the GEMV of the chunk two back has run. */
+            if (k >= 2 && (e = hipStreamWaitEvent(cs, ev->consumed[b], 0)) != hipSuccess)
+                return hip_fail(e, "sweep_staged: wait");
+            if (host_wait) {
+                if (!started && (e = hipEventSynchronize(ev->start)) != hipSuccess)
+                    return hip_fail(e, "sweep_staged: host wait");
+                started = true;
+                if (k >= 2 && (e = hipEventSynchronize(ev->consumed[b])) != hipSuccess)
+                    return hip_fail(e, "sweep_staged: host wait");
+            }
+            if (rows * code_row > 0 &&
+                (e = hipMemcpyAsync(buf[b], static_cast<const char*>(m.w) + r0 * code_row, (size_t)(rows * code_row),
+                                    hipMemcpyDefault, cs)) != hipSuccess)
+                return hip_fail(e, "sweep_staged: copy");
+            if (scale_row > 0 &&
+                (e = hipMemcpyAsync(buf[b] + soff, static_cast<const char*>(m.scales) + r0 * scale_row,
+                                    (size_t)(rows * scale_row), hipMemcpyDefault, cs)) != hipSuccess)
+                return hip_fail(e, "sweep_staged: copy");
+            if ((e = hipEventRecord(ev->copied[b], cs)) != hipSuccess || (e = hipStreamWaitEvent(s, ev->copied[b], 0)) != hipSuccess)
+                return hip_fail(e, "sweep_staged: ordering");
+            const DevMat d = make_devmat(m.fmt, rows, m.K, buf[b], scale_row > 0 ? buf[b] + soff : nullptr, x,
+                                         reinterpret_cast<float*>(y + r0 * 4));
+            if ((e = wsr::launch_gemv(d, s)) != hipSuccess) return hip_fail(e, "sweep_staged: launch");
+            if ((e = hipEventRecord(ev->consumed[b], s)) != hipSuccess) return hip_fail(e, "sweep_staged: ordering");
+        }
+    }
+    return ok();
+}
+
+wsr_status wsr_host_resident_pages(const void* host, size_t bytes, size_t* resident_pages, size_t* total_pages) {
+    if (!host || !resident_pages || !total_pages) return fail(WSR_E_ARG, "host_resident_pages: null pointer");
+    const long pg = sysconf(_SC_PAGESIZE);
+    const uintptr_t a = reinterpret_cast<uintptr_t>(host) / pg * pg;
+    const uintptr_t end = (reinterpret_cast<uintptr_t>(host) + bytes + pg - 1) / pg * pg;
+    const size_t np = (end - a) / pg;
+    std::vector<unsigned char> v(np ? np : 1);
+    if (np && mincore(reinterpret_cast<void*>(a), end - a, v.data()) != 0)
+        return fail(WSR_E_ARG, "host_resident_pages: range is not mapped");
+    size_t r = 0;
+    for (size_t i = 0; i < np; ++i) r += v[i] & 1;
+    *resident_pages = r;
+    *total_pages = np;
+    return ok();
+}
+
+wsr_status wsr_select_endpoint(const wsr_endpoint_probe* p, double theta, int32_t* choice, double* times_ms) {
+    if (!p || !choice) return fail(WSR_E_ARG, "select_endpoint: null pointer");
+    if (!(theta >= 0.0) || !(p->w_bytes > 0.0)) return fail(WSR_E_ARG, "select_endpoint: theta and W must be >= 0 and > 0");
+    if (p->excluded & ~((1u << WSR_EP_MAP) | (1u << WSR_EP_RESIDENT) | (1u << WSR_EP_COPY)))
+        return fail(WSR_E_ARG, "select_endpoint: unknown endpoint in the exclusion mask %#x", p->excluded);
+    const int eps[3] = {WSR_EP_MAP, WSR_EP_RESIDENT, WSR_EP_COPY};
+    double t[3];
+    for (int j = 0; j < 3; ++j) {
+        const double b = p->rate[j];
+        t[j] = b > 0.0 ? p->w_bytes / b * 1e3 : -1.0;
+        if (times_ms) times_ms[j] = t[j];
+    }
+    /* Storage-bound stop: the mapped set is not resident after prefaulting. */
+    if (!p->mapped_resident) {
+        *choice = WSR_EP_STORAGE_BOUND;
+        return ok();
+    }
+    bool live[3];
+    for (int j = 0; j < 3; ++j) live[j] = t[j] > 0.0 && !(p->excluded & (1u << eps[j]));
+    if (!p->resident_ok) live[1] = false;     /* allocation failed, or it evicted the mapping */
+    int best = -1;
+    for (int j = 0; j < 3; ++j)
+        if (live[j] && (best < 0 || t[j] < t[best])) best = j;
+    if (best < 0) {
+        *choice = WSR_EP_NONE;
+        return ok();
+    }
+    /* Tie band: mapping wins when its time is within theta of the fastest survivor. */
+    if (live[0] && t[0] - t[best] <= theta * t[best]) best = 0;
+    *choice = eps[best];
+    return ok();
 }
 
 }  // extern "C"

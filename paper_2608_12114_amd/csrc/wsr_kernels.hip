@@ -177,6 +177,9 @@ __global__ __launch_bounds__(BLOCK) void k_gemv_q4_cols(DevMat d) {
     rows_q4_cols<T>(d, r0, std::min<int64_t>(r0 + R, d.M), 0, lane);
 }
 
+/* One group of R rows per wave.  The full and the partial group take separate branches rather than
+   a clamp of the row end: the clamp's select was miscompiled (the pre-emit peephole dropped the
+   instruction that set the select's condition, so the end became r0 + R past the last row). */
 template <int T>
 __global__ __launch_bounds__(BLOCK) void k_gemv_i8(DevMat d) {
     constexpr int R = GemvI8<T>::R;
@@ -184,7 +187,8 @@ __global__ __launch_bounds__(BLOCK) void k_gemv_i8(DevMat d) {
     const int64_t wave = (int64_t)blockIdx.x * WAVES_PER_BLOCK + wave_in_block();
     const int64_t r0 = wave * R;
     if (r0 >= d.M) return;
-    rows_i8<T, R, GemvI8<T>::U>(d, r0, std::min<int64_t>(r0 + R, d.M), 0, lane);
+    if (d.M - r0 >= R) rows_i8<T, R, GemvI8<T>::U>(d, r0, r0 + R, 0, lane);
+    else rows_i8<T, 1, GemvI8<T>::U>(d, r0, d.M, 0, lane);
 }
 
 static hipError_t launch_gemv_i8(const DevMat& m, int T, hipStream_t s) {

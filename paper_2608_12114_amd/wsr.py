@@ -19,6 +19,8 @@ STATUS_NAMES = {0: "WSR_OK", 1: "WSR_E_ARG", 2: "WSR_E_ALIGN", 3: "WSR_E_SIZE",
 WSR_F16, WSR_BF16, WSR_Q4, WSR_I8 = 1, 2, 3, 4
 WSR_REG_READONLY, WSR_REG_PIN, WSR_REG_PREPINNED = 1, 2, 4
 WSR_MAT_AFTER_PREVIOUS = 1
+WSR_EP_NONE, WSR_EP_MAP, WSR_EP_RESIDENT, WSR_EP_COPY, WSR_EP_STORAGE_BOUND = range(5)
+ENDPOINT_NAMES = {0: "none", 1: "map", 2: "resident", 3: "copy", 4: "storage-bound"}
 
 
 class WsrError(RuntimeError):
@@ -33,6 +35,12 @@ class wsr_mat(ctypes.Structure):
                 ("w", ctypes.c_void_p), ("scales", ctypes.c_void_p),
                 ("x", ctypes.c_void_p), ("x_tok_stride", ctypes.c_int64),
                 ("y", ctypes.c_void_p), ("y_tok_stride", ctypes.c_int64)]
+
+
+class wsr_endpoint_probe(ctypes.Structure):
+    _fields_ = [("w_bytes", ctypes.c_double), ("rate", ctypes.c_double * 3),
+                ("mapped_resident", ctypes.c_int32), ("resident_ok", ctypes.c_int32),
+                ("excluded", ctypes.c_uint32), ("reserved", ctypes.c_int32)]
 
 
 if not os.path.exists(LIB_PATH):
@@ -64,10 +72,15 @@ _L.wsr_gemv_f16_cols.argtypes = [_vp, _vp, _i64, _vp, _i64, _i64, _i64, _i32, ct
 _L.wsr_decode_sweep_batched.argtypes = [ctypes.POINTER(wsr_mat), _i32, _i32, _i32, _vp, _sz, _vp]
 _L.wsr_gemv_q4_cols.argtypes = [_vp, _vp, _vp, _i64, _vp, _i64, _i64, _i64, _i32, _vp]
 _L.wsr_gemv_i8.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _vp]
+_L.wsr_sweep_staged.argtypes = [ctypes.POINTER(wsr_mat), _i32, _i32, _vp, _sz, _vp, _vp]
+_L.wsr_host_resident_pages.argtypes = [_vp, _sz, ctypes.POINTER(_sz), ctypes.POINTER(_sz)]
+_L.wsr_select_endpoint.argtypes = [ctypes.POINTER(wsr_endpoint_probe), ctypes.c_double, ctypes.POINTER(_i32),
+                                   ctypes.POINTER(ctypes.c_double)]
 _L.wsr_gemv_i8_cols.argtypes = [_vp, _vp, _vp, _i64, _vp, _i64, _i64, _i64, _i32, _vp]
 for _f in ("wsr_register_host", "wsr_unregister_host", "wsr_probe_read", "wsr_gemv_f16",
            "wsr_gemv_q4", "wsr_decode_sweep", "wsr_gemv_f16_cols", "wsr_decode_sweep_batched",
-           "wsr_gemv_q4_cols", "wsr_gemv_i8", "wsr_gemv_i8_cols"):
+           "wsr_gemv_q4_cols", "wsr_gemv_i8", "wsr_gemv_i8_cols", "wsr_sweep_staged", "wsr_host_resident_pages",
+           "wsr_select_endpoint"):
     getattr(_L, _f).restype = ctypes.c_int
 
 
@@ -180,3 +193,28 @@ def wsr_decode_sweep(mats, n_tokens: int, ws, ws_bytes: int, stream=None) -> Non
 
 def wsr_decode_sweep_batched(mats, n_tokens: int, batch: int, ws, ws_bytes: int, stream=None) -> None:
     _check(_L.wsr_decode_sweep_batched(mats, _n(mats), n_tokens, batch, _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def wsr_sweep_staged(mats, token: int, stage, stage_bytes: int, stream=None, copy_stream=None) -> None:
+    _check(_L.wsr_sweep_staged(mats, _n(mats), token, _ptr(stage), stage_bytes, _stream(stream),
+                               _stream(copy_stream)))
+
+
+def wsr_host_resident_pages(host, nbytes: int) -> tuple[int, int]:
+    """Returns (resident pages, pages spanned)."""
+    r, t = _sz(), _sz()
+    _check(_L.wsr_host_resident_pages(_ptr(host), nbytes, ctypes.byref(r), ctypes.byref(t)))
+    return r.value, t.value
+
+
+def wsr_select_endpoint(w_bytes: float, b_map: float, b_resident: float, b_copy: float, theta: float = 0.05,
+                        mapped_resident: bool = True, resident_ok: bool = True,
+                        excluded: int = 0) -> tuple[int, list[float]]:
+    """Alg. 2: returns (endpoint code, [W/B in ms for map, resident, copy]); rates in bytes/s, <= 0
+    for an endpoint not measured."""
+    p = wsr_endpoint_probe(w_bytes, (ctypes.c_double * 3)(b_map, b_resident, b_copy), int(bool(mapped_resident)),
+                           int(bool(resident_ok)), excluded, 0)
+    c = _i32()
+    t = (ctypes.c_double * 3)()
+    _check(_L.wsr_select_endpoint(ctypes.byref(p), theta, ctypes.byref(c), t))
+    return c.value, list(t)

@@ -21,13 +21,13 @@ def declared():
 
 def test_exports_every_declared_symbol():
     names = declared()
-    assert len(names) == 15, names
+    assert len(names) == 18, names
     for n in names:
         assert hasattr(L, n), n
 
 
 def test_version_and_status_values():
-    assert wsr.wsr_abi_version() == 2
+    assert wsr.wsr_abi_version() == 3
     m = re.search(r"#define WSR_ABI_VERSION (\d+)", HEADER)
     assert int(m.group(1)) == wsr.wsr_abi_version()
     for name, val in (("WSR_OK", 0), ("WSR_E_ARG", 1), ("WSR_E_ALIGN", 2), ("WSR_E_SIZE", 3),
@@ -156,6 +156,22 @@ def test_sweep_argument_checks():
         m = wsr.make_mats([good, bad])
         assert _status(f, m, 2, 1, A, ws, None) == st, bad
         assert "matrix 1" in wsr.wsr_last_error()
+
+
+def test_sweep_staged_argument_checks():
+    f = "wsr_sweep_staged"
+    good = dict(fmt=2, M=8, K=64, w=A, x=A, y=A, x_tok_stride=128, y_tok_stride=32)
+    mats = wsr.make_mats([good, dict(good, fmt=4, scales=A)])
+    assert _status(f, mats, 2, -1, A, 1 << 20, None, None) == wsr.WSR_E_ARG        # negative token
+    assert _status(f, mats, 2, 0, None, 1 << 20, None, None) == wsr.WSR_E_ARG      # no staging buffer
+    assert _status(f, mats, 2, 0, A + 16, 1 << 20, None, None) == wsr.WSR_E_ALIGN  # 256-byte alignment
+    assert _status(f, mats, 2, 0, A, 600, None, None) == wsr.WSR_E_SIZE            # a half holds no row
+    assert "holds no row" in wsr.wsr_last_error()
+    assert _status(f, mats, 0, 0, None, 0, None, None) == wsr.WSR_OK               # nothing to do
+    bad = wsr.make_mats([dict(good, fmt=3)])                                        # q4 without scales
+    assert _status(f, bad, 1, 0, A, 1 << 20, None, None) == wsr.WSR_E_ARG
+    bad = wsr.make_mats([dict(good, x_tok_stride=8)])
+    assert _status(f, bad, 1, 0, A, 1 << 20, None, None) == wsr.WSR_E_ALIGN
 
 
 def test_register_argument_checks():

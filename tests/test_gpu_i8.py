@@ -28,12 +28,12 @@ def inputs(M, K, seed, s0):
             synth.normal16(K, wl.X_SIGMA, "f16", seed=seed, stream=s0 + 2))
 
 
-# (3, 28672) faulted the GPU once, with the GEMV then using 8-row groups; the kernel's indexing
-# for that shape reads in bounds and no cause was found, so the case stays off the GPU and the
-# GEMV went back to the row table that had passed it.
-FAULTED = pytest.mark.skip(reason="faulted the GPU once with an earlier row table; cause not found, kept off the GPU")
+# (3, 28672) once faulted the GPU: the GEMV's row clamp min(r0 + R, M) was miscompiled to r0 + R, so
+# with 8-row groups a wave read 5 rows (140 KB) past the codes.  The kernel no longer clamps with a
+# select, the build rejects the miscompile, and tests/test_gpu_bounds.py checks that only rows < M
+# are written.
 SHAPES = [(1, 16), (5, 32), (37, 2064), (300, 4096), (4096, 4096), (1024, 14336), (14336, 4096),
-          pytest.param(3, 28672, marks=FAULTED), (12288, 7168)]
+          (3, 28672), (12288, 7168)]
 
 
 @pytest.mark.parametrize("M,K", SHAPES)
