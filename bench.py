@@ -12,6 +12,8 @@ Also measured in the same run and reported under "rows" (same JSON line):
   llama8b_q4   decode sweep of the Llama-3-8B shape in 4-bit blocks (4.22 GB per token)
   protocol     the matched protocol's pass: int8 GEMV with fp16 row scales over 12 matrices of
                12288 x 7168 (1.06 GB), as 12 dispatches and as one launch, plus the T-sweep
+  endpoints    Alg. 2 over the same set stored as a file: map (pinned pages in place), resident and
+               per-use copy (staged from the file pages) rates, and the endpoint it selects
   size_sweep   bf16 GEMV with K = 4096 and N = 256 ... 140800 rows, resident and host-mapped
   bus          pinned host -> device copy rate, the ceiling of every host-mapped arm
   copy         1 GiB elementwise read+write pass (calibrates the HBM byte counters; not default)
@@ -69,7 +71,7 @@ def parse():
     p.add_argument("--steps", type=int, default=16, help="timed decode tokens of the headline")
     p.add_argument("--warmup", type=int, default=2, help="untimed decode tokens before timing")
     p.add_argument("--workload", default="llama70b_bf16", choices=["llama70b_bf16", "llama8b_q4"])
-    p.add_argument("--rows", default="probe,gemv_f16,llama8b_q4,protocol,size_sweep,bus",
+    p.add_argument("--rows", default="probe,gemv_f16,llama8b_q4,protocol,endpoints,size_sweep,bus",
                    help="comma list of extra rows ('' for none)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time of the sample")
@@ -371,6 +373,116 @@ def row_protocol(stream, wsr, warmup_passes=12, passes=31, tokens=8):
     return res
 
 
+def row_endpoints(stream, wsr, warmup=2, passes=5, stage_mib=64):
+    """Alg. 2 (Sec. 8.1) on this machine, over the protocol's working set (12 int8 matrices of
+    12288 x 7168 with row scales, 1.06 GB) stored as a file: map and prefault the file, check its
+    residency, measure map, resident and per-use copy with the same row loops, check residency
+    again, and let the library's selection rank W / B with the 5 % band.  The GPU cannot read an
+    unregistered file mapping here and registering existing pages is refused on this platform, so
+    the map arm reads the same bytes in place from pinned host pages (Alg. 1's adoption of pages
+    that are already device-visible); the copy arm stages from the file pages themselves."""
+    import tempfile
+    import torch
+    import synth
+    from synth import device as dv
+    from synth import workloads as wl
+    mats = wl.protocol_matrices()
+    M, K = wl.PROTOCOL_M, wl.PROTOCOL_K
+    code_b, scale_b = M * K, M * 2
+    per = code_b + scale_b
+    W = per * len(mats)
+    page = os.sysconf("SC_PAGE_SIZE")
+    path = os.path.join(tempfile.gettempdir(), f"wsr_protocol_{os.getpid()}.bin")
+    res = {"working_set_bytes": W, "matrices": len(mats), "file": "codes then row scales per matrix"}
+    try:
+        t0 = time.time()
+        with open(path, "wb") as f:
+            for m in mats:
+                f.write(synth.i8_codes(M, K, seed=wl.SEED, stream=wl.w_stream(m.index)).tobytes())
+                f.write(synth.i8_scales(M, seed=wl.SEED, stream=wl.s_stream(m.index)).tobytes())
+        fmap = np.memmap(path, dtype=np.uint8, mode="r")
+        # step 1: prefault; step 2: residency of the mapped set
+        _ = int(fmap[::page].sum())
+        r_pages, t_pages = wsr.wsr_host_resident_pages(fmap.ctypes.data, W)
+        res["file_written_and_prefaulted_s"] = time.time() - t0
+        res["mapped_resident_pages"] = [r_pages, t_pages]
+        log(f"endpoints: {W / 1e9:.2f} GB file mapped, {r_pages}/{t_pages} pages resident")
+        xs = [dv.to_device(synth.normal16(K, wl.X_SIGMA, "f16", seed=wl.SEED,
+                                          stream=wl.x_stream(m.layer, wl.X_SLOTS[m.slot]))) for m in mats]
+        ys = {a: [torch.empty(M, dtype=torch.float32, device="cuda") for _ in mats] for a in ("map", "resident", "copy_file", "copy_pinned")}
+
+        def specs(base, arm):
+            return wsr.make_mats([dict(fmt=wsr.WSR_I8, M=M, K=K, w=base + i * per, scales=base + i * per + code_b,
+                                       x=xs[i], y=ys[arm][i]) for i in range(len(mats))])
+
+        def timed_arm(fn):
+            for _ in range(warmup):
+                fn()
+            torch.cuda.synchronize()
+            return float(np.median([timed(fn, 1, stream) for _ in range(passes)]))
+
+        # resident arm: one copy of the file pages into device memory, then the sweep over it
+        dev = torch.empty(W, dtype=torch.uint8, device="cuda")
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        dev.copy_(torch.from_numpy(np.asarray(fmap)))
+        torch.cuda.synchronize()
+        res["one_time_copy_s"] = time.perf_counter() - t1
+        sp_dev = specs(dev.data_ptr(), "resident")
+        ws = torch.zeros(wsr.wsr_sweep_workspace_bytes(sp_dev), dtype=torch.uint8, device="cuda")
+        t_res = timed_arm(lambda: wsr.wsr_decode_sweep(sp_dev, 1, ws, ws.numel(), stream))
+        # map arm: the same bytes read in place from pinned host pages, adopted through registration
+        pinned = torch.empty((W + page - 1) // page * page, dtype=torch.uint8, pin_memory=True)
+        pinned.numpy()[:W] = fmap
+        dview, granted = wsr.wsr_register_host(pinned, pinned.numel(), 0)
+        try:
+            sp_map = specs(dview, "map")
+            t_map = timed_arm(lambda: wsr.wsr_decode_sweep(sp_map, 1, ws, ws.numel(), stream))
+            # per-use copy: staged through 2 x stage_mib of device memory, from the file pages and
+            # from the pinned pages
+            stage = torch.empty(2 * stage_mib << 20, dtype=torch.uint8, device="cuda")
+            cs = torch.cuda.Stream()
+            sp_cf = specs(fmap.ctypes.data, "copy_file")
+            sp_cp = specs(pinned.data_ptr(), "copy_pinned")
+            t_cf = timed_arm(lambda: wsr.wsr_sweep_staged(sp_cf, 0, stage, stage.numel(), stream, cs))
+            t_cp = timed_arm(lambda: wsr.wsr_sweep_staged(sp_cp, 0, stage, stage.numel(), stream, cs))
+            torch.cuda.synchronize()
+        finally:
+            wsr.wsr_unregister_host(pinned)
+        same = all(torch.equal(ys["resident"][i], ys[a][i]) for a in ("map", "copy_file", "copy_pinned")
+                   for i in range(len(mats)))
+        # step 5: the mapping after one pass of every arm
+        r_after, _ = wsr.wsr_host_resident_pages(fmap.ctypes.data, W)
+        mapped_resident = r_pages == t_pages
+        resident_ok = r_after == t_pages
+        rates = {"map": W / t_map, "resident": W / t_res, "copy": W / t_cf}
+        res.update({
+            "GBps": {"map_pinned_in_place": W / t_map / 1e9, "resident": W / t_res / 1e9,
+                     "copy_from_file_pages": W / t_cf / 1e9, "copy_from_pinned": W / t_cp / 1e9},
+            "ms_per_pass": {"map": t_map * 1e3, "resident": t_res * 1e3, "copy_file": t_cf * 1e3,
+                            "copy_pinned": t_cp * 1e3},
+            "one_time_copy_GBps": W / res["one_time_copy_s"] / 1e9,
+            "register_granted": granted, "mapped_resident_pages_after": r_after,
+            "outputs_bitwise_equal_across_arms": bool(same), "stage_bytes": 2 * stage_mib << 20})
+        verdicts = {}
+        for theta in (0.02, 0.05, 0.10, 0.20):
+            code, times = wsr.wsr_select_endpoint(W, rates["map"], rates["resident"], rates["copy"], theta,
+                                                  mapped_resident, resident_ok)
+            verdicts[f"{theta:.2f}"] = wsr.ENDPOINT_NAMES[code]
+        res["alg2"] = {"theta": 0.05, "choice": verdicts["0.05"], "path_time_ms": dict(zip(("map", "resident", "copy"), times)),
+                       "theta_sweep": verdicts, "mapped_resident": mapped_resident, "resident_ok": resident_ok}
+        log(f"endpoints: map {W / t_map / 1e9:.1f} GB/s, resident {W / t_res / 1e9:.1f} GB/s, "
+            f"copy from file {W / t_cf / 1e9:.1f} GB/s (pinned {W / t_cp / 1e9:.1f}); one-time copy "
+            f"{res['one_time_copy_GBps']:.1f} GB/s; Alg. 2 -> {verdicts['0.05']} (theta 2-20 %: "
+            f"{sorted(set(verdicts.values()))}); outputs equal: {same}")
+        del dev, pinned, stage, ws, fmap
+        torch.cuda.empty_cache()
+    finally:
+        if os.path.exists(path):
+            os.remove(path)
+    return res
+
+
 def row_size_sweep(stream, wsr):
     import torch
     import synth
@@ -500,6 +612,8 @@ def main():
             rows[r] = row_size_sweep(stream, wsr)
         elif r == "protocol":
             rows[r] = row_protocol(stream, wsr)
+        elif r == "endpoints":
+            rows[r] = row_endpoints(stream, wsr)
         elif r == "bus":
             rows[r] = row_bus(stream)
         elif r == "copy":
