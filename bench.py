@@ -14,6 +14,8 @@ Also measured in the same run and reported under "rows" (same JSON line):
                12288 x 7168 (1.06 GB), as 12 dispatches and as one launch, plus the T-sweep
   endpoints    Alg. 2 over the same set stored as a file: map (pinned pages in place), resident and
                per-use copy (staged from the file pages) rates, and the endpoint it selects
+  ordering     the protocol pass ordered against an in-flight framework stream by four mechanisms
+               (in-stream, event, host-visible event, host drain): excess ms per pass
   size_sweep   bf16 GEMV with K = 4096 and N = 256 ... 140800 rows, resident and host-mapped
   bus          pinned host -> device copy rate, the ceiling of every host-mapped arm
   copy         1 GiB elementwise read+write pass (calibrates the HBM byte counters; not default)
@@ -71,7 +73,7 @@ def parse():
     p.add_argument("--steps", type=int, default=16, help="timed decode tokens of the headline")
     p.add_argument("--warmup", type=int, default=2, help="untimed decode tokens before timing")
     p.add_argument("--workload", default="llama70b_bf16", choices=["llama70b_bf16", "llama8b_q4"])
-    p.add_argument("--rows", default="probe,gemv_f16,llama8b_q4,protocol,endpoints,size_sweep,bus",
+    p.add_argument("--rows", default="probe,gemv_f16,llama8b_q4,protocol,endpoints,ordering,size_sweep,bus",
                    help="comma list of extra rows ('' for none)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time of the sample")
@@ -483,6 +485,88 @@ def row_endpoints(stream, wsr, warmup=2, passes=5, stage_mib=64):
     return res
 
 
+def row_ordering(stream, wsr, depths=(2, 8, 32), steps=20, reps=7, seed=0, workloads=("mm", "small")):
+    """Sec. 4.3's ordering hierarchy on HIP.  A step of a decode-like loop: the framework issues D
+    matrix products on its stream and then writes the pass's activation; the weight pass (the
+    protocol's 1.06 GB of int8, one launch) is ordered after that by one of four mechanisms; the
+    framework's next operation reads the pass's output.  Excess = time per step minus that of the
+    same loop without the pass, paired within each repetition; arms run in a shuffled order per
+    repetition.  The pass alone on an idle GPU is the floor of every excess."""
+    import torch
+    from synth import device as dv
+    from synth import workloads as wl
+    mats = wl.protocol_matrices()
+    inp = dv.SweepInputs(mats, [wl.I8] * len(mats), tokens=1)
+    specs = wsr.make_mats(inp.specs())
+    ws = torch.zeros(wsr.wsr_sweep_workspace_bytes(specs), dtype=torch.uint8, device="cuda")
+    fs, own = torch.cuda.Stream(), torch.cuda.Stream()
+    a = torch.randn(2048, 2048, device="cuda", dtype=torch.bfloat16)
+    small = torch.zeros(1 << 14, device="cuda")
+    x0 = next(iter(inp.x.values()))[0][0]          # the activation the framework writes
+    xsrc = x0.clone()
+    acc = torch.zeros(16, device="cuda")
+    rng = np.random.default_rng(seed)
+    modes = {"none": None, "in-stream": wsr.WSR_ORDER_STREAM, "event": wsr.WSR_ORDER_EVENT,
+             "host-visible event": wsr.WSR_ORDER_HOST_EVENT, "host drain": wsr.WSR_ORDER_DRAIN}
+
+    def run(mode, depth, n, work):
+        for _ in range(n):
+            with torch.cuda.stream(fs):
+                if work == "mm":
+                    b = a
+                    for _ in range(depth):
+                        b = torch.mm(b, a)
+                else:
+                    for _ in range(depth):
+                        small.add_(1.0)
+                x0.copy_(xsrc)
+            if mode is not None:
+                wsr.wsr_decode_sweep_ordered(specs, 1, ws, ws.numel(), fs, own, mode)
+            with torch.cuda.stream(fs):
+                acc.add_(inp.y[0][0, :16])
+
+    pass_alone = median_of(lambda: wsr.wsr_decode_sweep(specs, 1, ws, ws.numel(), stream), 1, 15, stream)
+    op_ms = {}
+    with torch.cuda.stream(fs):
+        op_ms["mm"] = median_of(lambda: torch.mm(a, a), 8, 5, fs) / 8 * 1e3
+        op_ms["small"] = median_of(lambda: small.add_(1.0), 64, 5, fs) / 64 * 1e3
+    res = {"pass_alone_ms": pass_alone * 1e3, "steps": steps, "repetitions": reps,
+           "workloads": {"mm": "bf16 mm 2048 x 2048 x 2048 (GPU-bound: the host enqueues faster than the GPU runs)",
+                         "small": "in-place add on 16K floats (launch-bound: the GPU runs as fast as the host enqueues)"},
+           "op_gpu_ms": op_ms, "results": {},
+           "paper_context_ms": {"in-stream": 0.33, "event": 0.44, "host-visible event": 3.46,
+                                "host drain": 5.80, "note": "Apple M5 Max and Metal; another machine"}}
+    for work in workloads:
+        for depth in depths:
+            for m in modes.values():
+                run(m, depth, 2, work)
+            torch.cuda.synchronize()
+            excess = {k: [] for k in modes if k != "none"}
+            base = []
+            for _ in range(reps):
+                order = list(modes)
+                rng.shuffle(order)
+                t = {}
+                for k in order:
+                    torch.cuda.synchronize()
+                    t0 = time.perf_counter()
+                    run(modes[k], depth, steps, work)
+                    torch.cuda.synchronize()
+                    t[k] = (time.perf_counter() - t0) / steps
+                base.append(t["none"] * 1e3)
+                for k in excess:
+                    excess[k].append((t[k] - t["none"]) * 1e3)
+            row = {k: {"median_ms": float(np.median(v)), "iqr_ms": [float(np.percentile(v, 25)), float(np.percentile(v, 75))]}
+                   for k, v in excess.items()}
+            res["results"][f"{work}/{depth}"] = {"step_without_pass_ms": float(np.median(base)), "excess": row}
+            log(f"ordering, {work} x {depth} per step ({np.median(base):.3f} ms without the pass): " +
+                ", ".join(f"{k} {v['median_ms']:.3f}" for k, v in row.items()) +
+                f" ms (pass alone {pass_alone * 1e3:.3f} ms)")
+    del specs, ws, inp, a
+    torch.cuda.empty_cache()
+    return res
+
+
 def row_size_sweep(stream, wsr):
     import torch
     import synth
@@ -614,6 +698,8 @@ def main():
             rows[r] = row_protocol(stream, wsr)
         elif r == "endpoints":
             rows[r] = row_endpoints(stream, wsr)
+        elif r == "ordering":
+            rows[r] = row_ordering(stream, wsr)
         elif r == "bus":
             rows[r] = row_bus(stream)
         elif r == "copy":

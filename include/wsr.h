@@ -196,6 +196,27 @@ wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, vo
 wsr_status wsr_decode_sweep_batched(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch,
                                     void* ws, size_t ws_bytes, void* stream);
 
+/* ---- ordering against a framework stream (execution contract C3, Table 1; Sec. 4.3) -----------
+
+   wsr_decode_sweep_ordered: the outputs of wsr_decode_sweep, with the pass ordered after all work
+   already enqueued on `framework_stream` and all later work on `framework_stream` ordered after the
+   pass, by one of four mechanisms (Sec. 4.3 compares their cost under an in-flight workload):
+     WSR_ORDER_STREAM      the pass is enqueued on framework_stream itself (own_stream unused);
+     WSR_ORDER_EVENT       the pass runs on own_stream, which waits on the GPU for an event
+                           recorded on framework_stream;
+     WSR_ORDER_HOST_EVENT  as WSR_ORDER_EVENT, but the host waits for that event before it
+                           enqueues the pass (the signal becomes host-visible; the call blocks);
+     WSR_ORDER_DRAIN       the host drains the whole device (hipDeviceSynchronize) first.
+   In the last three, framework_stream then waits on the GPU for an event recorded after the pass.
+   Only WSR_ORDER_STREAM and WSR_ORDER_EVENT keep every dependency on the GPU.  Calls on one
+   device are serialised while they enqueue (events shared per device). */
+#define WSR_ORDER_STREAM 0
+#define WSR_ORDER_EVENT 1
+#define WSR_ORDER_HOST_EVENT 2
+#define WSR_ORDER_DRAIN 3
+wsr_status wsr_decode_sweep_ordered(const wsr_mat* mats, int32_t n, int32_t n_tokens, void* ws, size_t ws_bytes,
+                                    void* framework_stream, void* own_stream, int32_t mode);
+
 /* ---- per-use copy endpoint (Sec. 8.1; Table 2, pipelined double-buffered copy; Sec. 7.2,
    overlapped streaming) ---------------------------------------------------------------------
 

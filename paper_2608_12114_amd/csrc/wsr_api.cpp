@@ -308,8 +308,22 @@ size_t wsr_sweep_workspace_bytes(const wsr_mat* mats, int32_t n) {
 
 namespace {
 
-wsr_status sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch, void* ws,
-                 size_t ws_bytes, void* stream) {
+struct Seg {
+    int first, count, fmt;
+    int64_t total;
+};
+
+/* A checked sweep: the device table and the launch groups (segments between
+   WSR_MAT_AFTER_PREVIOUS flags). */
+struct SweepPlan {
+    std::vector<DevMat> tab;
+    std::vector<Seg> segs;
+    int32_t batch = 1;
+};
+
+/* Every check of a sweep; enqueues nothing. */
+wsr_status plan_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch, void* ws,
+                      size_t ws_bytes, SweepPlan& p) {
     if (n < 0 || n_tokens < 1) return fail(WSR_E_ARG, "decode_sweep: n=%d n_tokens=%d", n, n_tokens);
     if (batch != 1 && batch != 2 && batch != 4 && batch != 8 && batch != 16)
         return fail(WSR_E_ARG, "decode_sweep: batch=%d must be 1, 2, 4, 8 or 16", batch);
@@ -319,9 +333,8 @@ wsr_status sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch
     const size_t need = wsr_sweep_workspace_bytes(mats, n);
     if (ws_bytes < need) return fail(WSR_E_SIZE, "decode_sweep: workspace %zu < %zu bytes", ws_bytes, need);
 
-    std::vector<DevMat> tab((size_t)n);
-    struct Seg { int first, count, fmt; int64_t total; };
-    std::vector<Seg> segs;
+    p.tab.assign((size_t)n, DevMat{});
+    p.segs.clear();
     char who[64];
     for (int32_t i = 0; i < n; ++i) {
         const wsr_mat& m = mats[i];
@@ -335,8 +348,8 @@ wsr_status sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch
             return fail(WSR_E_SIZE, "%s: token strides overflow", who);
         if (batch > 1 && m.M > 0 && m.y_tok_stride < m.M * 4)
             return fail(WSR_E_ARG, "%s: tokens of one pass would share outputs (y_tok_stride < 4 M)", who);
-        if (segs.empty() || (m.flags & WSR_MAT_AFTER_PREVIOUS)) segs.push_back(Seg{i, 0, m.fmt, 0});
-        Seg& g = segs.back();
+        if (p.segs.empty() || (m.flags & WSR_MAT_AFTER_PREVIOUS)) p.segs.push_back(Seg{i, 0, m.fmt, 0});
+        Seg& g = p.segs.back();
         DevMat d = make_devmat(m.fmt, m.M, m.K, m.w, m.scales, m.x, m.y);
         d.x_stride = m.x_tok_stride;
         d.y_stride = m.y_tok_stride;
@@ -346,29 +359,43 @@ wsr_status sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch
         g.total += d.M * d.row_bytes;
         if (g.fmt != m.fmt) g.fmt = 0;
         g.count += 1;
-        tab[(size_t)i] = d;
+        p.tab[(size_t)i] = d;
     }
+    /* Passes of `batch` tokens, at most 8 when the table holds q4 or int8 matrices. */
+    for (int32_t i = 0; i < n && batch > 8; ++i)
+        if (mats[i].fmt == WSR_Q4 || mats[i].fmt == WSR_I8) batch = 8;
+    p.batch = batch;
+    return ok();
+}
+
+/* Enqueue a planned sweep (n > 0) on `stream`. */
+wsr_status run_sweep(const SweepPlan& p, int32_t n, int32_t n_tokens, void* ws, void* stream) {
     hipStream_t s = static_cast<hipStream_t>(stream);
     unsigned* ctr = static_cast<unsigned*>(ws);
     DevMat* dtab = reinterpret_cast<DevMat*>(static_cast<char*>(ws) + wsr::SWEEP_CTR_BYTES);
     int64_t* dcost = reinterpret_cast<int64_t*>(reinterpret_cast<char*>(dtab) +
                                                 ((size_t)n * sizeof(DevMat) + 255) / 256 * 256);
-    hipError_t e = wsr::launch_put_table(dtab, dcost, tab.data(), n, ctr, s);
+    hipError_t e = wsr::launch_put_table(dtab, dcost, p.tab.data(), n, ctr, s);
     if (e != hipSuccess) return hip_fail(e, "decode_sweep: table upload");
-    /* Passes of `batch` tokens (at most 8 when the table holds q4 matrices); the last tokens go in
-       passes of the largest power of two that fits. */
-    for (int32_t i = 0; i < n && batch > 8; ++i)
-        if (mats[i].fmt == WSR_Q4 || mats[i].fmt == WSR_I8) batch = 8;
+    /* The last tokens go in passes of the largest power of two that fits. */
     for (int32_t t = 0; t < n_tokens;) {
-        int32_t T = batch;
+        int32_t T = p.batch;
         while (T > n_tokens - t) T >>= 1;
-        for (const Seg& g : segs) {
+        for (const Seg& g : p.segs) {
             e = wsr::launch_sweep(dtab + g.first, dcost + g.first, g.count, g.total, g.fmt, t, T, ctr, s);
             if (e != hipSuccess) return hip_fail(e, "decode_sweep: launch");
         }
         t += T;
     }
     return ok();
+}
+
+wsr_status sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch, void* ws,
+                 size_t ws_bytes, void* stream) {
+    SweepPlan p;
+    wsr_status st = plan_sweep(mats, n, n_tokens, batch, ws, ws_bytes, p);
+    if (st != WSR_OK || n == 0) return st;
+    return run_sweep(p, n, n_tokens, ws, stream);
 }
 
 }  // namespace
@@ -574,6 +601,63 @@ wsr_status wsr_select_endpoint(const wsr_endpoint_probe* p, double theta, int32_
     /* Tie band: mapping wins when its time is within theta of the fastest survivor. */
     if (live[0] && t[0] - t[best] <= theta * t[best]) best = 0;
     *choice = eps[best];
+    return ok();
+}
+
+}  // extern "C"
+
+/* ---- a decode pass ordered against another stream (execution contract C3, Sec. 4.3) ----------- */
+
+namespace {
+
+struct OrderEvents {
+    std::mutex mu;
+    bool made = false;
+    hipEvent_t before{}, after{};
+};
+OrderEvents g_order_ev[64];
+
+}  // namespace
+
+extern "C" {
+
+wsr_status wsr_decode_sweep_ordered(const wsr_mat* mats, int32_t n, int32_t n_tokens, void* ws, size_t ws_bytes,
+                                    void* framework_stream, void* own_stream, int32_t mode) {
+    if (mode < WSR_ORDER_STREAM || mode > WSR_ORDER_DRAIN)
+        return fail(WSR_E_ARG, "decode_sweep_ordered: unknown mode %d", mode);
+    if (mode == WSR_ORDER_STREAM) return sweep(mats, n, n_tokens, 1, ws, ws_bytes, framework_stream);
+    SweepPlan p;
+    wsr_status st = plan_sweep(mats, n, n_tokens, 1, ws, ws_bytes, p);
+    if (st != WSR_OK || n == 0) return st;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "decode_sweep_ordered: device");
+    if (dev < 0 || dev >= 64) return fail(WSR_E_ARG, "decode_sweep_ordered: device %d", dev);
+    OrderEvents& ev = g_order_ev[dev];
+    std::lock_guard<std::mutex> lock(ev.mu);
+    if (!ev.made) {
+        if ((e = hipEventCreateWithFlags(&ev.before, hipEventDisableTiming)) != hipSuccess ||
+            (e = hipEventCreateWithFlags(&ev.after, hipEventDisableTiming)) != hipSuccess)
+            return hip_fail(e, "decode_sweep_ordered: events");
+        ev.made = true;
+    }
+    hipStream_t fs = static_cast<hipStream_t>(framework_stream), os = static_cast<hipStream_t>(own_stream);
+    /* Before the pass: the framework's work so far must be complete. */
+    if (mode == WSR_ORDER_DRAIN) {
+        if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "decode_sweep_ordered: drain");
+    } else {
+        if ((e = hipEventRecord(ev.before, fs)) != hipSuccess) return hip_fail(e, "decode_sweep_ordered: record");
+        if (mode == WSR_ORDER_EVENT)
+            e = hipStreamWaitEvent(os, ev.before, 0);
+        else
+            e = hipEventSynchronize(ev.before);       /* the host observes the signal */
+        if (e != hipSuccess) return hip_fail(e, "decode_sweep_ordered: wait");
+    }
+    st = run_sweep(p, n, n_tokens, ws, own_stream);
+    if (st != WSR_OK) return st;
+    /* After the pass: the framework's later work waits for it on the GPU. */
+    if ((e = hipEventRecord(ev.after, os)) != hipSuccess || (e = hipStreamWaitEvent(fs, ev.after, 0)) != hipSuccess)
+        return hip_fail(e, "decode_sweep_ordered: order after");
     return ok();
 }
 

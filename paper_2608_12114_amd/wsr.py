@@ -19,6 +19,8 @@ STATUS_NAMES = {0: "WSR_OK", 1: "WSR_E_ARG", 2: "WSR_E_ALIGN", 3: "WSR_E_SIZE",
 WSR_F16, WSR_BF16, WSR_Q4, WSR_I8 = 1, 2, 3, 4
 WSR_REG_READONLY, WSR_REG_PIN, WSR_REG_PREPINNED = 1, 2, 4
 WSR_MAT_AFTER_PREVIOUS = 1
+WSR_ORDER_STREAM, WSR_ORDER_EVENT, WSR_ORDER_HOST_EVENT, WSR_ORDER_DRAIN = range(4)
+ORDER_NAMES = {0: "in-stream", 1: "event", 2: "host-visible event", 3: "host drain"}
 WSR_EP_NONE, WSR_EP_MAP, WSR_EP_RESIDENT, WSR_EP_COPY, WSR_EP_STORAGE_BOUND = range(5)
 ENDPOINT_NAMES = {0: "none", 1: "map", 2: "resident", 3: "copy", 4: "storage-bound"}
 
@@ -73,13 +75,14 @@ _L.wsr_decode_sweep_batched.argtypes = [ctypes.POINTER(wsr_mat), _i32, _i32, _i3
 _L.wsr_gemv_q4_cols.argtypes = [_vp, _vp, _vp, _i64, _vp, _i64, _i64, _i64, _i32, _vp]
 _L.wsr_gemv_i8.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _vp]
 _L.wsr_sweep_staged.argtypes = [ctypes.POINTER(wsr_mat), _i32, _i32, _vp, _sz, _vp, _vp]
+_L.wsr_decode_sweep_ordered.argtypes = [ctypes.POINTER(wsr_mat), _i32, _i32, _vp, _sz, _vp, _vp, _i32]
 _L.wsr_host_resident_pages.argtypes = [_vp, _sz, ctypes.POINTER(_sz), ctypes.POINTER(_sz)]
 _L.wsr_select_endpoint.argtypes = [ctypes.POINTER(wsr_endpoint_probe), ctypes.c_double, ctypes.POINTER(_i32),
                                    ctypes.POINTER(ctypes.c_double)]
 _L.wsr_gemv_i8_cols.argtypes = [_vp, _vp, _vp, _i64, _vp, _i64, _i64, _i64, _i32, _vp]
 for _f in ("wsr_register_host", "wsr_unregister_host", "wsr_probe_read", "wsr_gemv_f16",
            "wsr_gemv_q4", "wsr_decode_sweep", "wsr_gemv_f16_cols", "wsr_decode_sweep_batched",
-           "wsr_gemv_q4_cols", "wsr_gemv_i8", "wsr_gemv_i8_cols", "wsr_sweep_staged", "wsr_host_resident_pages",
+           "wsr_gemv_q4_cols", "wsr_gemv_i8", "wsr_gemv_i8_cols", "wsr_sweep_staged", "wsr_host_resident_pages", "wsr_decode_sweep_ordered",
            "wsr_select_endpoint"):
     getattr(_L, _f).restype = ctypes.c_int
 
@@ -218,3 +221,8 @@ def wsr_select_endpoint(w_bytes: float, b_map: float, b_resident: float, b_copy:
     t = (ctypes.c_double * 3)()
     _check(_L.wsr_select_endpoint(ctypes.byref(p), theta, ctypes.byref(c), t))
     return c.value, list(t)
+
+
+def wsr_decode_sweep_ordered(mats, n_tokens: int, ws, ws_bytes: int, framework_stream, own_stream, mode: int) -> None:
+    _check(_L.wsr_decode_sweep_ordered(mats, _n(mats), n_tokens, _ptr(ws), ws_bytes, _stream(framework_stream),
+                                       _stream(own_stream), mode))

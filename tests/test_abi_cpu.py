@@ -21,7 +21,7 @@ def declared():
 
 def test_exports_every_declared_symbol():
     names = declared()
-    assert len(names) == 18, names
+    assert len(names) == 19, names
     for n in names:
         assert hasattr(L, n), n
 
@@ -172,6 +172,20 @@ def test_sweep_staged_argument_checks():
     assert _status(f, bad, 1, 0, A, 1 << 20, None, None) == wsr.WSR_E_ARG
     bad = wsr.make_mats([dict(good, x_tok_stride=8)])
     assert _status(f, bad, 1, 0, A, 1 << 20, None, None) == wsr.WSR_E_ALIGN
+
+
+def test_sweep_ordered_argument_checks():
+    f = "wsr_decode_sweep_ordered"
+    good = dict(fmt=2, M=8, K=64, w=A, x=A, y=A, x_tok_stride=128, y_tok_stride=32)
+    mats = wsr.make_mats([good])
+    ws = wsr.wsr_sweep_workspace_bytes(mats)
+    for mode in (-1, 4):
+        assert _status(f, mats, 1, 1, A, ws, None, None, mode) == wsr.WSR_E_ARG
+    for mode in (1, 2, 3):
+        assert _status(f, mats, 1, 0, A, ws, None, None, mode) == wsr.WSR_E_ARG      # n_tokens < 1
+        assert _status(f, mats, 1, 1, A, ws - 1, None, None, mode) == wsr.WSR_E_SIZE
+        assert _status(f, mats, 0, 1, None, 0, None, None, mode) == wsr.WSR_OK       # empty sweep
+    assert _status(f, mats, 1, 0, A, ws, None, None, 0) == wsr.WSR_E_ARG             # in-stream: sweep's checks
 
 
 def test_register_argument_checks():
