@@ -237,21 +237,25 @@ hipError_t launch_gemv(const DevMat& m, hipStream_t s) {
 
 /* ======================================= sweep ================================================ */
 
-constexpr int TABLE_CHUNK = 16;
+/* Matrices per table-upload launch.  The chunk travels as a by-value kernel argument (30.7 KB at
+   320 entries; arguments of up to 32,000 bytes were checked to arrive intact on this stack), so one
+   launch uploads the table of a 225-matrix model and the arguments are captured by value when a
+   caller records the sweep into a graph. */
+constexpr int TABLE_CHUNK = 320;
 struct TableChunk {
     int32_t n;
     int32_t pad_[3];
     DevMat m[TABLE_CHUNK];
 };
+static_assert(sizeof(TableChunk) <= 31 * 1024, "table chunk must stay within the checked argument size");
 
-__global__ __launch_bounds__(WAVE) void k_put_table(DevMat* __restrict__ dst, int64_t* __restrict__ cost,
-                                                    TableChunk c, unsigned* __restrict__ ctr) {
-    const int i = threadIdx.x;
-    if (i < c.n) {
+__global__ __launch_bounds__(BLOCK) void k_put_table(DevMat* __restrict__ dst, int64_t* __restrict__ cost,
+                                                     TableChunk c, unsigned* __restrict__ ctr) {
+    for (int i = threadIdx.x; i < c.n; i += BLOCK) {
         dst[i] = c.m[i];
         cost[i] = c.m[i].cost0;
     }
-    if (ctr && i < 2) ctr[i] = 0u;
+    if (ctr && threadIdx.x < 2) ctr[threadIdx.x] = 0u;
 }
 
 hipError_t launch_put_table(DevMat* dst, int64_t* cost, const DevMat* src, int n, unsigned* ctr,
@@ -260,7 +264,7 @@ hipError_t launch_put_table(DevMat* dst, int64_t* cost, const DevMat* src, int n
         TableChunk c{};
         c.n = std::min(TABLE_CHUNK, n - first);
         for (int i = 0; i < c.n; ++i) c.m[i] = src[first + i];
-        hipLaunchKernelGGL(k_put_table, dim3(1), dim3(WAVE), 0, s, dst + first, cost + first, c,
+        hipLaunchKernelGGL(k_put_table, dim3(1), dim3(BLOCK), 0, s, dst + first, cost + first, c,
                            first == 0 ? ctr : nullptr);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
@@ -346,14 +350,14 @@ static int cu_count() {
 }
 
 /* 16-bit weights: tiles, 4 rows x 4 KiB steps per wave, one block (4 waves) per CU (few, long
-   streams).  q4: spans of about 64 KiB per wave, 8 rows x 1 block per lane per step (eight rows
+   streams).  q4: spans of about 48 KiB per wave, 8 rows x 1 block per lane per step (eight rows
    share each block's activation decode), two register sets in flight; the grid is sized so that
-   blocks retire and are replaced throughout the token (16,100 blocks for 4.2 GB).  int8: spans of
+   blocks retire and are replaced throughout the token (21,500 blocks for 4.2 GB).  int8: spans of
    about SWEEP_SPAN_I8[T] bytes per wave with 8 rows x 1 chunk per lane per step and, for one
    column, three register sets in flight; tiles with one block per CU reach about half the rate
    (one wave per SIMD cannot cover the latency at each row group's start). */
 constexpr int SWEEP_BLOCKS_PER_CU_16 = 1;
-constexpr int64_t SWEEP_SPAN_Q4 = 64 << 10;
+constexpr int64_t SWEEP_SPAN_Q4 = 48 << 10;
 constexpr int64_t SWEEP_SPAN_I8[4] = {32 << 10, 32 << 10, 128 << 10, 128 << 10};   /* T = 1, 2, 4, 8 */
 
 /* Grid of a span-scheduled sweep: about `span` bytes per wave, at least one wave per SIMD. */
