@@ -196,6 +196,20 @@ wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, vo
 wsr_status wsr_decode_sweep_batched(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch,
                                     void* ws, size_t ws_bytes, void* stream);
 
+/* ---- batched decode on the matrix cores (Sec. 3.4, 5.2: several activation columns per weight read) -
+
+   wsr_decode_sweep_mma: for t < n_tokens and every matrix m, y_m(t) = W_m . x_m(t) as in
+   wsr_decode_sweep, with up to 16 tokens per pass over the weights and the products formed by the
+   matrix cores (v_mfma_f32_16x16x32): each 16-row, 16-token tile accumulates slabs of 32 weights,
+   decoded to exact fp16 integers for q4 and int8 and used as stored for fp16 and bf16.  Every
+   product is exact and sums are fp32, but a slab's products are added in the matrix core's own
+   order, so outputs agree with wsr_decode_sweep within rounding (not bit for bit); a unit
+   activation vector still returns the dequantised weights exactly.  Tokens go in passes of 16, the
+   last pass holding the rest.  Formats, layouts, flags and the workspace as for wsr_decode_sweep;
+   with n_tokens > 1 every matrix must have y_tok_stride >= 4 M. */
+wsr_status wsr_decode_sweep_mma(const wsr_mat* mats, int32_t n, int32_t n_tokens, void* ws, size_t ws_bytes,
+                                void* stream);
+
 /* ---- ordering against a framework stream (execution contract C3, Table 1; Sec. 4.3) -----------
 
    wsr_decode_sweep_ordered: the outputs of wsr_decode_sweep, with the pass ordered after all work

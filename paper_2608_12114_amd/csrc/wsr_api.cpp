@@ -606,6 +606,35 @@ wsr_status wsr_select_endpoint(const wsr_endpoint_probe* p, double theta, int32_
 
 }  // extern "C"
 
+/* ---- matrix-core sweep ---------------------------------------------------------------------------- */
+
+extern "C" wsr_status wsr_decode_sweep_mma(const wsr_mat* mats, int32_t n, int32_t n_tokens, void* ws, size_t ws_bytes,
+                                           void* stream) {
+    SweepPlan p;
+    wsr_status st = plan_sweep(mats, n, n_tokens, n_tokens > 1 ? 16 : 1, ws, ws_bytes, p);
+    if (st != WSR_OK || n == 0) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    unsigned* ctr = static_cast<unsigned*>(ws);
+    DevMat* dtab = reinterpret_cast<DevMat*>(static_cast<char*>(ws) + wsr::SWEEP_CTR_BYTES);
+    int64_t* dcost = reinterpret_cast<int64_t*>(reinterpret_cast<char*>(dtab) +
+                                                ((size_t)n * sizeof(DevMat) + 255) / 256 * 256);
+    hipError_t e = wsr::launch_put_table(dtab, dcost, p.tab.data(), n, ctr, s);
+    if (e != hipSuccess) return hip_fail(e, "decode_sweep_mma: table upload");
+    std::vector<int64_t> max_group(p.segs.size(), 0);
+    for (size_t i = 0; i < p.segs.size(); ++i)
+        for (int m = p.segs[i].first; m < p.segs[i].first + p.segs[i].count; ++m)
+            max_group[i] = std::max(max_group[i], p.tab[m].row_bytes * std::min(p.tab[m].M, wsr::mma_group_rows()));
+    for (int32_t t = 0; t < n_tokens; t += 16) {
+        const int ntok = std::min<int32_t>(16, n_tokens - t);
+        for (size_t i = 0; i < p.segs.size(); ++i) {
+            const Seg& g = p.segs[i];
+            e = wsr::launch_sweep_mma(dtab + g.first, dcost + g.first, g.count, g.total, max_group[i], g.fmt, t, ntok, s);
+            if (e != hipSuccess) return hip_fail(e, "decode_sweep_mma: launch");
+        }
+    }
+    return ok();
+}
+
 /* ---- a decode pass ordered against another stream (execution contract C3, Sec. 4.3) ----------- */
 
 namespace {

@@ -872,13 +872,9 @@ __device__ __forceinline__ void rows_q4(const DevMat& d, int64_t r0, int64_t r1,
 
 __device__ __forceinline__ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-template <int FMT, int R16, int U16, int RQ, int UQ, int QNB = 2, int T = 1, int RC = Cols16<T>::R,
-          int UC = Cols16<T>::U, int RQC = Cols4<(T <= 8 ? T : 8)>::R>
-__device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, const int64_t* __restrict__ cost,
-                                             int nmat, int64_t lo, int64_t hi, int32_t token, int lane,
-                                             int& hint) {
-    /* Last matrix whose stream starts at or before lo: from the hint when it still holds, else by
-       bisection over the dense offset array (8 bytes per matrix, so it stays in the scalar cache). */
+/* Last matrix whose stream starts at or before byte lo: from the hint when it still holds, else by
+   bisection over the dense offset array (8 bytes per matrix, so it stays in the scalar cache). */
+__device__ __forceinline__ int first_matrix(const int64_t* __restrict__ cost, int nmat, int64_t lo, int hint) {
     int a = hint;
     if (cost[a] > lo) a = 0;
     if (a + 1 < nmat && cost[a + 1] <= lo) {
@@ -888,17 +884,35 @@ __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, con
             if (cost[mid] <= lo) a = mid; else b = mid - 1;
         }
     }
-    for (int m = a; m < nmat; ++m) {
+    return a;
+}
+
+/* Rows [r0, r1) of matrix d that the byte range [lo, hi) of the weight stream covers.  A byte
+   boundary maps to the first group of g rows starting at or after it, the same way for the ranges
+   on both sides, so the ranges still cover each row once and break only between whole groups. */
+struct RowRange {
+    int64_t r0, r1;
+};
+__device__ __forceinline__ RowRange range_rows(const DevMat& d, int64_t lo, int64_t hi, int64_t g) {
+    const int64_t r0 = lo > d.cost0 ? ceil_div(lo - d.cost0, d.row_bytes * g) * g : 0;
+    const int64_t e1 = ceil_div(hi - d.cost0, d.row_bytes * g) * g;
+    return RowRange{r0, d.M < e1 ? d.M : e1};
+}
+
+template <int FMT, int R16, int U16, int RQ, int UQ, int QNB = 2, int T = 1, int RC = Cols16<T>::R,
+          int UC = Cols16<T>::U, int RQC = Cols4<(T <= 8 ? T : 8)>::R>
+__device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, const int64_t* __restrict__ cost,
+                                             int nmat, int64_t lo, int64_t hi, int32_t token, int lane,
+                                             int& hint) {
+    for (int m = first_matrix(cost, nmat, lo, hint); m < nmat; ++m) {
         const DevMat d = tab[m];
         if (d.cost0 >= hi) break;
         hint = m;
         const int fmt = FMT ? FMT : d.fmt;
-        /* A byte boundary maps to the first row group starting at or after it, the same way for
-           the ranges on both sides, so the ranges still cover each row once and break only
-           between whole groups of R rows. */
         const int64_t g = fmt == FMT_Q4 ? (T == 1 ? RQ : RQC)
                         : fmt == FMT_I8 ? ColsI8<(T <= 8 ? T : 8)>::R
                                         : (T == 1 ? R16 : RC);
+        /* range_rows' mapping, written out here: as a call it changes this loop's code. */
         const int64_t r0 = lo > d.cost0 ? ceil_div(lo - d.cost0, d.row_bytes * g) * g : 0;
         const int64_t e1 = ceil_div(hi - d.cost0, d.row_bytes * g) * g;
         const int64_t r1 = d.M < e1 ? d.M : e1;
@@ -922,6 +936,265 @@ __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, con
                 else if ((FMT == 0 || FMT == FMT_I8) && fmt == FMT_I8) rows_i8<T>(d, r0, r1, token, lane);
             }
         }
+    }
+}
+
+/* ---- matrix-core rows: up to 16 tokens per pass over the weights ----------------------------------
+
+   With several tokens per pass the packed dot products of the loops above cost one instruction per
+   weight pair per token, and from about four tokens on the vector ALUs, not HBM, set the rate.
+   These loops hand the products to the matrix cores instead.  A wave owns tiles of 16 rows; per
+   32-element slab of K it forms D = X^T W^T for the tile with one v_mfma_f32_16x16x32: the A
+   operand holds 16 token columns of activations (columns past the pass's tokens are zero), the B
+   operand 16 weight rows decoded to fp16.  Decoded weights are exact: q4 and int8 codes become the
+   small integers q as 1024 + (q + bias) formed by one bit operation, minus 1024 + bias by one packed
+   fp16 subtraction; 16-bit weights are used as stored.  Every product q x is exact in fp32, and
+   the scales multiply the fp32 slab sums, but the matrix core adds a slab's products in an order of
+   its own, so these results agree with the other loops within rounding, not bit for bit.
+   Operand layout (checked on the device): lane i holds A[i%16][8(i/16)+j], B[8(i/16)+j][i%16] and
+   D[4(i/16)+j][i%16].  K may be permuted inside a slab as long as A and B follow the same order;
+   the decoders give (k0,k4,k1,k5,k2,k6,k3,k7) for a q4 word and (k0,k2,k1,k3,k4,k6,k5,k7) for two
+   int8 words, and the activation loaders permute x to match.  A q4 scale covers one block of 32, so
+   a slab is one block: the four words a lane loaded (block b0 + i/16 of row i%16) are transposed
+   between the four 16-lane groups with two rounds of lane swaps, and each block's product is formed
+   alone and added with its row's scale.  int8 scales are per row and multiply the finished sum. */
+typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 b8_t __attribute__((ext_vector_type(8)));
+typedef float f4_t __attribute__((ext_vector_type(4)));
+
+constexpr int MMA_TOKENS = 16;              /* token columns per tile                               */
+
+template <int FMT>
+__device__ __forceinline__ f4_t mma16(u32x4 a, u32x4 b, f4_t c) {
+    if constexpr (FMT == FMT_BF16)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(b8_t, a), __builtin_bit_cast(b8_t, b), c,
+                                                       0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, a), __builtin_bit_cast(h8_t, b), c,
+                                                      0, 0, 0);
+}
+
+/* v - bias in both fp16 halves of a word holding 1024 + v (exact for the small integers here). */
+__device__ __forceinline__ uint32_t f16_sub_bias(uint32_t v, uint32_t neg_bias) {
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(h2_t, v) + __builtin_bit_cast(h2_t, neg_bias));
+}
+
+/* One q4 code word (code k in nibble k) as 8 fp16 integers, order (k0,k4,k1,k5,k2,k6,k3,k7). */
+__device__ __forceinline__ u32x4 q4_word_f16(uint32_t w) {
+    constexpr uint32_t M = 0x000F000Fu, E = 0x64086408u, NEG = 0xE408E408u;   /* 1024 + (code ^ 8); -1032 */
+    return u32x4{f16_sub_bias((w & M) ^ E, NEG), f16_sub_bias(((w >> 4) & M) ^ E, NEG),
+                 f16_sub_bias(((w >> 8) & M) ^ E, NEG), f16_sub_bias(((w >> 12) & M) ^ E, NEG)};
+}
+
+/* Two int8 code words (codes k0..k3, k4..k7) as 8 fp16 integers, order (k0,k2,k1,k3,k4,k6,k5,k7). */
+__device__ __forceinline__ u32x4 i8_words_f16(uint32_t w0, uint32_t w1) {
+    constexpr uint32_t M = 0x00FF00FFu, E = 0x64806480u, NEG = 0xE480E480u;   /* 1024 + (code ^ 128); -1152 */
+    return u32x4{f16_sub_bias((w0 & M) ^ E, NEG), f16_sub_bias(((w0 >> 8) & M) ^ E, NEG),
+                 f16_sub_bias((w1 & M) ^ E, NEG), f16_sub_bias(((w1 >> 8) & M) ^ E, NEG)};
+}
+
+/* Eight activations x0..x7 (16 bytes) in the q4 decoder's order and in the int8 decoder's order. */
+__device__ __forceinline__ u32x4 x8_q4_order(u32x4 u) {
+    return u32x4{__builtin_amdgcn_perm(u.z, u.x, 0x05040100u), __builtin_amdgcn_perm(u.z, u.x, 0x07060302u),
+                 __builtin_amdgcn_perm(u.w, u.y, 0x05040100u), __builtin_amdgcn_perm(u.w, u.y, 0x07060302u)};
+}
+__device__ __forceinline__ u32x4 x8_i8_order(u32x4 u) {
+    return u32x4{__builtin_amdgcn_perm(u.y, u.x, 0x05040100u), __builtin_amdgcn_perm(u.y, u.x, 0x07060302u),
+                 __builtin_amdgcn_perm(u.w, u.z, 0x05040100u), __builtin_amdgcn_perm(u.w, u.z, 0x07060302u)};
+}
+
+/* Lane group g (lanes 16g .. 16g + 15) holds the four words of block g in w; afterwards it holds
+   word g of blocks 0, 1, 2, 3 in w.x, w.y, w.z, w.w (a 4 x 4 transpose between the groups). */
+__device__ __forceinline__ u32x4 transpose_groups(u32x4 w) {
+    const auto s02 = __builtin_amdgcn_permlane32_swap(w.x, w.z, false, false);
+    const auto s13 = __builtin_amdgcn_permlane32_swap(w.y, w.w, false, false);
+    const auto s01 = __builtin_amdgcn_permlane16_swap(s02[0], s13[0], false, false);
+    const auto s23 = __builtin_amdgcn_permlane16_swap(s02[1], s13[1], false, false);
+    return u32x4{s01[0], s01[1], s23[0], s23[1]};
+}
+
+/* K elements per step of the matrix-core loops, and slabs (matrix instructions) per step. */
+template <int FMT> struct MmaStep { static constexpr int K = 128, SLABS = 4; };
+template <> struct MmaStep<FMT_I8> { static constexpr int K = 64, SLABS = 2; };
+
+/* Registers of one unit (a group of NT tiles, one step of K): the activations of each slab, the
+   code or weight chunks of each tile, and the scales (q4: the step's four block scales of each
+   tile's row; int8: each tile's row scale). */
+template <int FMT, int NT>
+struct MmaUnit {
+    static constexpr int SL = MmaStep<FMT>::SLABS;
+    static constexpr int WC = (FMT == FMT_Q4 || FMT == FMT_I8) ? 1 : 4;   /* 16-byte chunks per tile */
+    u32x4 x[SL];
+    u32x4 w[NT][WC];
+    uint32_t s[NT][2];
+};
+
+__device__ __forceinline__ u32x4 keep_if(bool ok, u32x4 v) { return ok ? v : zero4(); }
+
+/* Rows [r0, r1) of matrix d for tokens token0 .. token0 + ntok - 1 (ntok <= 16), NT tiles of 16
+   rows per group.  The units (group, step) run as a two-set register pipeline, as in rows_q4: the
+   loads of the next unit are in flight while the current one is multiplied.  Every load is
+   unconditional with its address clamped into the operand: rows past r1 read row r1 - 1 and are
+   not stored, token slots past ntok read the first token and are not stored, and the values past
+   the row's end are zeroed when the ragged last step of K is multiplied (masking them as they
+   arrive would make each load wait at once).  q4 reads the four block scales of a step as one
+   8-byte load where the rows hold a multiple of 4 blocks and the scales are 8-byte aligned
+   (SCALE8); otherwise it reads them one by one. */
+template <int FMT, int NT, bool SCALE8>
+__device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1, int32_t token0, int ntok, int lane) {
+    using Unit = MmaUnit<FMT, NT>;
+    constexpr int SK = MmaStep<FMT>::K, SL = Unit::SL, WC = Unit::WC;
+    const int c = lane & 15, g = lane >> 4;                      /* token slot and tile row; group  */
+    g_u32x4* x = as_global<g_u32x4*>(static_cast<const char*>(d.x) + (int64_t)(token0 + (c < ntok ? c : 0)) * d.x_stride);
+    g_u32x4* Wq = as_global<g_u32x4*>(d.w);
+    g_u16* S = as_global<g_u16*>(d.s);
+    const int64_t nc = d.nc;                                     /* blocks (q4) or 16-byte chunks    */
+    const int64_t kelem = FMT == FMT_Q4 ? nc * 32 : FMT == FMT_I8 ? nc * 16 : nc * 8;
+    const int64_t steps = (kelem + SK - 1) / SK;
+    const int64_t ngroups = (r1 - r0 + 16 * NT - 1) / (16 * NT);
+    const int64_t n = ngroups * steps;                           /* units */
+    if (n == 0) return;
+    f4_t acc[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[t] = f4_t{0.f, 0.f, 0.f, 0.f};
+    int64_t gl = 0, kl = 0;                                      /* next unit to load     */
+    int64_t gc = 0, kc = 0;                                      /* next unit to multiply */
+    auto load = [&](Unit& u) {
+        const int64_t i0 = r0 + gl * 16 * NT, k0 = kl * SK;
+#pragma unroll
+        for (int j = 0; j < SL; ++j) {
+            const int64_t ke = FMT == FMT_I8 ? k0 + 16 * g + 8 * j : k0 + 32 * j + 8 * g;
+            u.x[j] = load_reused(x + std::min<int64_t>(ke, kelem - 8) / 8);
+        }
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const int64_t row = std::min<int64_t>(i0 + 16 * t + c, r1 - 1);
+            if constexpr (FMT == FMT_Q4) {
+                const int64_t b = k0 / 32 + g;                   /* this group's block */
+                u.w[t][0] = load_once(Wq + row * nc + std::min<int64_t>(b, nc - 1));
+                const int64_t b0 = k0 / 32;
+                if constexpr (SCALE8) {
+                    const uint64_t v = *reinterpret_cast<__attribute__((address_space(1))) const uint64_t*>(S + row * nc + b0);
+                    u.s[t][0] = (uint32_t)v;
+                    u.s[t][1] = (uint32_t)(v >> 32);
+                } else {
+                    uint32_t h[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) h[j] = S[row * nc + std::min<int64_t>(b0 + j, nc - 1)];
+                    u.s[t][0] = h[0] | h[1] << 16;
+                    u.s[t][1] = h[2] | h[3] << 16;
+                }
+            } else if constexpr (FMT == FMT_I8) {
+                const int64_t ch = k0 / 16 + g;
+                u.w[t][0] = load_once(Wq + row * nc + std::min<int64_t>(ch, nc - 1));
+                u.s[t][0] = S[row];
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int64_t ke = k0 + 32 * j + 8 * g;
+                    u.w[t][j] = load_once(Wq + row * nc + std::min<int64_t>(ke, kelem - 8) / 8);
+                }
+            }
+        }
+        if (++kl == steps) { kl = 0; ++gl; }
+    };
+    auto multiply = [&](Unit& u) {
+        const int64_t i0 = r0 + gc * 16 * NT, k0 = kc * SK;
+        if (k0 + SK > kelem) {                                   /* the ragged last step of K */
+#pragma unroll
+            for (int j = 0; j < SL; ++j) {
+                const int64_t ke = FMT == FMT_I8 ? k0 + 16 * g + 8 * j : k0 + 32 * j + 8 * g;
+                u.x[j] = keep_if(ke < kelem, u.x[j]);
+                if constexpr (WC == 4) {
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) u.w[t][j] = keep_if(ke < kelem, u.w[t][j]);
+                }
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            if constexpr (FMT == FMT_Q4) {
+                const u32x4 w = transpose_groups(u.w[t][0]);
+                const uint32_t wj[4] = {w.x, w.y, w.z, w.w};
+                const uint16_t sh[4] = {(uint16_t)u.s[t][0], (uint16_t)(u.s[t][0] >> 16), (uint16_t)u.s[t][1],
+                                        (uint16_t)(u.s[t][1] >> 16)};
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const float sc = k0 / 32 + j < nc ? f16_bits_to_f32(sh[j]) : 0.f;
+                    const f4_t p = mma16<FMT_F16>(x8_q4_order(u.x[j]), q4_word_f16(wj[j]), f4_t{0.f, 0.f, 0.f, 0.f});
+                    acc[t] += sc * p;
+                }
+            } else if constexpr (FMT == FMT_I8) {
+                acc[t] = mma16<FMT_F16>(x8_i8_order(u.x[0]), i8_words_f16(u.w[t][0].x, u.w[t][0].y), acc[t]);
+                acc[t] = mma16<FMT_F16>(x8_i8_order(u.x[1]), i8_words_f16(u.w[t][0].z, u.w[t][0].w), acc[t]);
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[t] = mma16<FMT>(u.x[j], u.w[t][j], acc[t]);
+            }
+        }
+        if (kc + 1 == steps) {                                   /* end of a group: store, reset */
+            /* lane (c, g) holds tokens 4 g .. 4 g + 3 of row c of each tile */
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const int64_t r = i0 + 16 * t + c;
+                float rs = 1.f;
+                if constexpr (FMT == FMT_I8) rs = f16_bits_to_f32((uint16_t)u.s[t][0]);
+                if (r < r1) {
+#pragma unroll
+                    for (int jj = 0; jj < 4; ++jj) {
+                        const int tok = 4 * g + jj;
+                        if (tok < ntok)                          /* a global (not flat) store keeps the load waits exact */
+                            as_global<g_f32*>(reinterpret_cast<char*>(d.y) + (int64_t)(token0 + tok) * d.y_stride)[r] =
+                                acc[t][jj] * rs;
+                    }
+                }
+                acc[t] = f4_t{0.f, 0.f, 0.f, 0.f};
+            }
+        }
+        if (++kc == steps) { kc = 0; ++gc; }
+    };
+    Unit buf[2];
+    load(buf[0]);
+    int64_t u = 0;                                               /* buf[0] holds unit u */
+    for (; u + 3 <= n; u += 2) {
+        load(buf[1]);                                            /* unit u + 1 */
+        __builtin_amdgcn_sched_barrier(0);
+        multiply(buf[0]);                                        /* unit u     */
+        load(buf[0]);                                            /* unit u + 2 */
+        __builtin_amdgcn_sched_barrier(0);
+        multiply(buf[1]);                                        /* unit u + 1 */
+    }
+    /* one or two units left, unit u in buf[0] */
+    if (u + 1 < n) {
+        load(buf[1]);
+        multiply(buf[0]);
+        multiply(buf[1]);
+    } else {
+        multiply(buf[0]);
+    }
+}
+
+/* The matrix-core sweep over the byte range [lo, hi) of the weight stream (groups of 16 NT rows). */
+template <int FMT, int NT>
+__device__ __forceinline__ void stream_range_mma(const DevMat* __restrict__ tab, const int64_t* __restrict__ cost,
+                                                 int nmat, int64_t lo, int64_t hi, int32_t token0, int ntok,
+                                                 int lane, int& hint) {
+    for (int m = first_matrix(cost, nmat, lo, hint); m < nmat; ++m) {
+        const DevMat d = tab[m];
+        if (d.cost0 >= hi) break;
+        hint = m;
+        const int fmt = FMT ? FMT : d.fmt;
+        const RowRange rr = range_rows(d, lo, hi, 16 * NT);
+        if (rr.r0 >= rr.r1) continue;
+        if ((FMT == 0 || FMT == FMT_F16) && fmt == FMT_F16)
+            rows_mma<FMT_F16, NT, false>(d, rr.r0, rr.r1, token0, ntok, lane);
+        else if ((FMT == 0 || FMT == FMT_BF16) && fmt == FMT_BF16)
+            rows_mma<FMT_BF16, NT, false>(d, rr.r0, rr.r1, token0, ntok, lane);
+        else if ((FMT == 0 || FMT == FMT_Q4) && fmt == FMT_Q4) {
+            if (d.nc % 4 == 0 && (reinterpret_cast<uintptr_t>(d.s) & 7) == 0) rows_mma<FMT_Q4, NT, true>(d, rr.r0, rr.r1, token0, ntok, lane);
+            else rows_mma<FMT_Q4, NT, false>(d, rr.r0, rr.r1, token0, ntok, lane);
+        } else if ((FMT == 0 || FMT == FMT_I8) && fmt == FMT_I8)
+            rows_mma<FMT_I8, NT, false>(d, rr.r0, rr.r1, token0, ntok, lane);
     }
 }
 

@@ -75,6 +75,7 @@ _L.wsr_decode_sweep_batched.argtypes = [ctypes.POINTER(wsr_mat), _i32, _i32, _i3
 _L.wsr_gemv_q4_cols.argtypes = [_vp, _vp, _vp, _i64, _vp, _i64, _i64, _i64, _i32, _vp]
 _L.wsr_gemv_i8.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _vp]
 _L.wsr_sweep_staged.argtypes = [ctypes.POINTER(wsr_mat), _i32, _i32, _vp, _sz, _vp, _vp]
+_L.wsr_decode_sweep_mma.argtypes = [ctypes.POINTER(wsr_mat), _i32, _i32, _vp, _sz, _vp]
 _L.wsr_decode_sweep_ordered.argtypes = [ctypes.POINTER(wsr_mat), _i32, _i32, _vp, _sz, _vp, _vp, _i32]
 _L.wsr_host_resident_pages.argtypes = [_vp, _sz, ctypes.POINTER(_sz), ctypes.POINTER(_sz)]
 _L.wsr_select_endpoint.argtypes = [ctypes.POINTER(wsr_endpoint_probe), ctypes.c_double, ctypes.POINTER(_i32),
@@ -82,7 +83,7 @@ _L.wsr_select_endpoint.argtypes = [ctypes.POINTER(wsr_endpoint_probe), ctypes.c_
 _L.wsr_gemv_i8_cols.argtypes = [_vp, _vp, _vp, _i64, _vp, _i64, _i64, _i64, _i32, _vp]
 for _f in ("wsr_register_host", "wsr_unregister_host", "wsr_probe_read", "wsr_gemv_f16",
            "wsr_gemv_q4", "wsr_decode_sweep", "wsr_gemv_f16_cols", "wsr_decode_sweep_batched",
-           "wsr_gemv_q4_cols", "wsr_gemv_i8", "wsr_gemv_i8_cols", "wsr_sweep_staged", "wsr_host_resident_pages", "wsr_decode_sweep_ordered",
+           "wsr_gemv_q4_cols", "wsr_gemv_i8", "wsr_gemv_i8_cols", "wsr_sweep_staged", "wsr_host_resident_pages", "wsr_decode_sweep_ordered", "wsr_decode_sweep_mma",
            "wsr_select_endpoint"):
     getattr(_L, _f).restype = ctypes.c_int
 
@@ -226,3 +227,7 @@ def wsr_select_endpoint(w_bytes: float, b_map: float, b_resident: float, b_copy:
 def wsr_decode_sweep_ordered(mats, n_tokens: int, ws, ws_bytes: int, framework_stream, own_stream, mode: int) -> None:
     _check(_L.wsr_decode_sweep_ordered(mats, _n(mats), n_tokens, _ptr(ws), ws_bytes, _stream(framework_stream),
                                        _stream(own_stream), mode))
+
+
+def wsr_decode_sweep_mma(mats, n_tokens: int, ws, ws_bytes: int, stream=None) -> None:
+    _check(_L.wsr_decode_sweep_mma(mats, _n(mats), n_tokens, _ptr(ws), ws_bytes, _stream(stream)))

@@ -21,7 +21,7 @@ def declared():
 
 def test_exports_every_declared_symbol():
     names = declared()
-    assert len(names) == 19, names
+    assert len(names) == 20, names
     for n in names:
         assert hasattr(L, n), n
 
@@ -186,6 +186,18 @@ def test_sweep_ordered_argument_checks():
         assert _status(f, mats, 1, 1, A, ws - 1, None, None, mode) == wsr.WSR_E_SIZE
         assert _status(f, mats, 0, 1, None, 0, None, None, mode) == wsr.WSR_OK       # empty sweep
     assert _status(f, mats, 1, 0, A, ws, None, None, 0) == wsr.WSR_E_ARG             # in-stream: sweep's checks
+
+
+def test_sweep_mma_argument_checks():
+    f = "wsr_decode_sweep_mma"
+    good = dict(fmt=3, M=8, K=64, w=A, scales=A, x=A, y=A, x_tok_stride=128, y_tok_stride=32)
+    mats = wsr.make_mats([good])
+    ws = wsr.wsr_sweep_workspace_bytes(mats)
+    assert _status(f, mats, 1, 0, A, ws, None) == wsr.WSR_E_ARG                  # n_tokens < 1
+    assert _status(f, mats, 1, 1, A, ws - 1, None) == wsr.WSR_E_SIZE
+    assert _status(f, mats, 0, 4, None, 0, None) == wsr.WSR_OK                   # empty sweep
+    shared = wsr.make_mats([dict(good, y_tok_stride=16)])
+    assert _status(f, shared, 1, 2, A, ws, None) == wsr.WSR_E_ARG                # tokens would share y
 
 
 def test_register_argument_checks():

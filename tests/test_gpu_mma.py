@@ -1,0 +1,139 @@
+"""Batched decode on the matrix cores (wsr_decode_sweep_mma): unit activation vectors return the
+dequantised weights bit for bit (which pins the decoders, the lane transposes and the operand
+orders), every token of a mixed-format sweep matches the oracle and the vector-ALU sweep, outputs
+outside the tokens and rows asked for stay untouched, and the full-size models agree on sampled rows."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from synth import device as dv
+from synth import workloads as wl
+from gpu_util import TOL, f32_bits, needs_gpu, rel_l2, stream, zeros_u8
+
+from paper_2608_12114_amd import wsr
+
+pytestmark = [pytest.mark.gpu, needs_gpu]
+CODE = {wl.F16: wsr.WSR_F16, wl.BF16: wsr.WSR_BF16, wl.Q4: wsr.WSR_Q4, wl.I8: wsr.WSR_I8}
+# K past a whole number of steps (128 elements; 64 for int8) and M past whole 64-row groups
+SHAPES = {wl.F16: (100, 520), wl.BF16: (77, 4104), wl.Q4: (100, 2080), wl.I8: (130, 2064)}
+
+
+def host_matrix(fmt, M, K, seed):
+    if fmt == wl.Q4:
+        return synth.q4_codes(M, K, seed=seed, stream=601), synth.q4_scales(M, K, seed=seed, stream=602)
+    if fmt == wl.I8:
+        return synth.i8_codes(M, K, seed=seed, stream=601), synth.i8_scales(M, seed=seed, stream=602)
+    return synth.normal16((M, K), wl.W_SIGMA, fmt, seed=seed, stream=601), None
+
+
+def run_mma(fmt, W, S, X, M, K, T, y_rows=None):
+    """X: (tokens, K) fp16/bf16 bits on the host; returns y (tokens_alloc, y_rows) after one call."""
+    y_rows = y_rows or M
+    w, s, x = dv.to_device(W), (dv.to_device(S) if S is not None else None), dv.to_device(X)
+    y = torch.full((X.shape[0], y_rows), float("nan"), dtype=torch.float32, device="cuda")
+    mats = wsr.make_mats([dict(fmt=CODE[fmt], M=M, K=K, w=w, scales=s, x=x, x_tok_stride=K * 2, y=y,
+                               y_tok_stride=y_rows * 4)])
+    ws = zeros_u8(wsr.wsr_sweep_workspace_bytes(mats))
+    wsr.wsr_decode_sweep_mma(mats, T, ws, ws.numel(), stream())
+    torch.cuda.synchronize()
+    return y.cpu().numpy()
+
+
+@pytest.mark.parametrize("fmt", [wl.F16, wl.BF16, wl.Q4, wl.I8])
+def test_mma_unit_vectors_exact(fmt):
+    M, K = SHAPES[fmt]
+    W, S = host_matrix(fmt, M, K, seed=7)
+    xfmt = wl.BF16 if fmt == wl.BF16 else wl.F16
+    zero, one = synth.encode16([0.0, 1.0], xfmt)
+    cols = [0, 1, 4, 5, 7, 8, 15, 16, 31, 32, 33, 63, 64, 127, 128, K - 1]
+    X = np.full((16, K), zero, np.uint16)
+    for t, j in enumerate(cols):
+        X[t, j] = one
+    y = run_mma(fmt, W, S, X, M, K, 16)
+    ora = oracle.get()
+    for t, j in enumerate(cols):
+        if fmt in (wl.Q4, wl.I8):
+            want = ora.gemv(dict(fmt=fmt, w=W, s=S), X[t])
+        else:
+            want = ora.gemv16(W, X[t], fmt)
+        assert np.array_equal(f32_bits(y[t]), f32_bits(want)), (fmt, j)
+
+
+@pytest.mark.parametrize("fmt", [wl.F16, wl.BF16, wl.Q4, wl.I8])
+@pytest.mark.parametrize("T", [1, 3, 16, 21])
+def test_mma_matrix_parity_and_bounds(fmt, T):
+    """T tokens in passes of 16; rows in a strided output (gaps after each token's M rows) and the
+    tokens past T stay NaN."""
+    M, K = SHAPES[fmt]
+    W, S = host_matrix(fmt, M, K, seed=8)
+    xfmt = wl.BF16 if fmt == wl.BF16 else wl.F16
+    X = synth.normal16((T + 2, K), wl.X_SIGMA, xfmt, seed=8, stream=603)
+    y = run_mma(fmt, W, S, X, M, K, T, y_rows=M + 5)
+    assert np.isnan(y[:, M:]).all() and np.isnan(y[T:]).all()
+    ora = oracle.get()
+    for t in range(T):
+        want = ora.gemv(dict(fmt=fmt, w=W, s=S), X[t]) if fmt in (wl.Q4, wl.I8) else ora.gemv16(W, X[t], fmt)
+        assert rel_l2(y[t, :M], want) <= TOL, (fmt, t)
+
+
+def sweep_pair(inp, tokens):
+    """(vector-ALU sweep outputs, matrix-core sweep outputs) for the same inputs."""
+    mats = wsr.make_mats(inp.specs())
+    ws = zeros_u8(wsr.wsr_sweep_workspace_bytes(mats))
+    for y in inp.y:
+        y.fill_(float("nan"))
+    wsr.wsr_decode_sweep(mats, tokens, ws, ws.numel(), stream())
+    torch.cuda.synchronize()
+    valu = [y.clone() for y in inp.y]
+    for y in inp.y:
+        y.fill_(float("nan"))
+    wsr.wsr_decode_sweep_mma(mats, tokens, ws, ws.numel(), stream())
+    torch.cuda.synchronize()
+    return valu, [y.clone() for y in inp.y]
+
+
+def test_mma_mixed_sweep():
+    mats = wl.decode_matrices(dv.small_model(layers=4, d=512, ffn=1536, vocab=3000))
+    fmts = [(wl.I8, wl.Q4, wl.BF16, wl.F16, wl.Q4)[m.layer] for m in mats]
+    inp = dv.SweepInputs(mats, fmts, tokens=19)
+    valu, mma = sweep_pair(inp, 19)
+    ora = oracle.get()
+    for i, (m, fmt) in enumerate(zip(mats, fmts)):
+        a, b = valu[i].cpu().numpy(), mma[i].cpu().numpy()
+        for t in range(19):
+            assert rel_l2(b[t], a[t]) <= 1e-5, (m.name, m.layer, t)
+        for t in (0, 15, 16, 18):
+            hw = inp.host_weights(i)
+            x = inp.host_x(i, t)
+            want = ora.gemv(dict(fmt=fmt, w=hw[0], s=hw[1]), x) if fmt in (wl.Q4, wl.I8) else ora.gemv16(hw, x, fmt)
+            assert rel_l2(b[t], want) <= TOL, (m.name, m.layer, t)
+
+
+@pytest.mark.parametrize("name", ["llama3-8b-q4", "llama-70b-bf16", "protocol-i8"])
+def test_mma_full_size(name):
+    """The full models, 16 tokens in one pass: every matrix against the vector-ALU sweep, and
+    sampled rows of every matrix against the oracle for the first and last token."""
+    if name == "protocol-i8":
+        mats, fmt = wl.protocol_matrices(), wl.I8
+    else:
+        _, shape, fmt = {"llama3-8b-q4": wl.LLAMA8B_Q4, "llama-70b-bf16": wl.LLAMA70B_BF16}[name]
+        mats = wl.decode_matrices(shape)
+    inp = dv.SweepInputs(mats, [fmt] * len(mats), tokens=16)
+    valu, mma = sweep_pair(inp, 16)
+    ora = oracle.get()
+    for i, m in enumerate(mats):
+        assert rel_l2(mma[i].cpu().numpy(), valu[i].cpu().numpy()) <= 1e-5, (m.name, m.layer)
+        rows = np.unique(np.linspace(0, m.M - 1, 4).astype(np.int64))
+        for t in (0, 15):
+            x = inp.host_x(i, t)
+            got = mma[i][t].cpu().numpy()[rows]
+            want = []
+            for r in rows:
+                hw = inp.host_weights(i, int(r), 1)
+                want.append((ora.gemv(dict(fmt=fmt, w=hw[0], s=hw[1]), x) if fmt in (wl.Q4, wl.I8)
+                             else ora.gemv16(hw, x, fmt))[0])
+            assert rel_l2(got, np.array(want)) <= TOL, (m.name, m.layer, t)
+    del inp, valu, mma
+    torch.cuda.empty_cache()
