@@ -206,7 +206,9 @@ wsr_status wsr_decode_sweep_batched(const wsr_mat* mats, int32_t n, int32_t n_to
    order, so outputs agree with wsr_decode_sweep within rounding (not bit for bit); a unit
    activation vector still returns the dequantised weights exactly.  Tokens go in passes of 16, the
    last pass holding the rest.  Formats, layouts, flags and the workspace as for wsr_decode_sweep;
-   with n_tokens > 1 every matrix must have y_tok_stride >= 4 M. */
+   with n_tokens > 1 every matrix must have y_tok_stride >= 4 M.  A row may hold at most 32 MiB of
+   weights or codes and x_tok_stride may be at most 128 MiB (WSR_E_SIZE otherwise): the kernels
+   address 64 rows and 16 tokens with 32-bit offsets. */
 wsr_status wsr_decode_sweep_mma(const wsr_mat* mats, int32_t n, int32_t n_tokens, void* ws, size_t ws_bytes,
                                 void* stream);
 

@@ -19,8 +19,11 @@ COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", f"-I{INCLUDE}", f"-I{CSRC}"]
 # feature; that is expected).
 # The atomic optimizer turns a single-lane atomic with a return value into a wave-wide scan that
 # consumes the result at once; the sweep's tile claims are issued ahead of use and must stay plain.
+# Matrix instructions write ordinary vector registers (not the accumulation registers), so their
+# results are scaled and summed without a copy out first.
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-          "-ffp-contract=fast", "-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]
+          "-ffp-contract=fast", "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
+          "-mllvm", "-amdgpu-mfma-vgpr-form"]
 
 
 # A toolchain hazard checked on every build.  The AMDGPU backend's pre-emit peephole deletes an

@@ -613,6 +613,9 @@ extern "C" wsr_status wsr_decode_sweep_mma(const wsr_mat* mats, int32_t n, int32
     SweepPlan p;
     wsr_status st = plan_sweep(mats, n, n_tokens, n_tokens > 1 ? 16 : 1, ws, ws_bytes, p);
     if (st != WSR_OK || n == 0) return st;
+    for (int32_t i = 0; i < n; ++i)       /* 64 rows and 16 tokens within 32-bit lane offsets */
+        if (p.tab[i].nc * 16 > (int64_t{1} << 25) || p.tab[i].x_stride > (int64_t{1} << 27))
+            return fail(WSR_E_SIZE, "decode_sweep_mma: matrix %d: rows above 32 MiB or x_tok_stride above 128 MiB", i);
     hipStream_t s = static_cast<hipStream_t>(stream);
     unsigned* ctr = static_cast<unsigned*>(ws);
     DevMat* dtab = reinterpret_cast<DevMat*>(static_cast<char*>(ws) + wsr::SWEEP_CTR_BYTES);

@@ -1013,123 +1013,186 @@ __device__ __forceinline__ u32x4 transpose_groups(u32x4 w) {
     return u32x4{s01[0], s01[1], s23[0], s23[1]};
 }
 
-/* K elements per step of the matrix-core loops, and slabs (matrix instructions) per step. */
-template <int FMT> struct MmaStep { static constexpr int K = 128, SLABS = 4; };
-template <> struct MmaStep<FMT_I8> { static constexpr int K = 64, SLABS = 2; };
+/* One step of the matrix-core loops.  Each lane reads J 16-byte chunks of its row per tile, chunk
+   jj of lane group g at byte 64 jj + 16 g of the step, so a load instruction covers 64 contiguous
+   bytes of each of 16 rows and a step 64 J bytes of every row.  HBM delivers about half its rate
+   when a wave reads only 64 bytes of a row per step, so q4 and int8 take two chunks.  SLABS is the
+   number of matrix instructions per tile and step, K the weights per row and step. */
+template <int FMT> struct MmaStep { static constexpr int J = 4, SLABS = 4, K = 128; };    /* 8 per chunk   */
+template <> struct MmaStep<FMT_Q4> { static constexpr int J = 2, SLABS = 8, K = 256; };   /* 32 per chunk  */
+template <> struct MmaStep<FMT_I8> { static constexpr int J = 2, SLABS = 4, K = 128; };   /* 16 per chunk  */
 
-/* Registers of one unit (a group of NT tiles, one step of K): the activations of each slab, the
-   code or weight chunks of each tile, and the scales (q4: the step's four block scales of each
-   tile's row; int8: each tile's row scale). */
+/* Registers of one unit (a group of NT tiles, one step): the activations of each slab, the chunks
+   of each tile, and the scales (q4: the step's eight block scales of each tile's row, as fp16
+   pairs; int8: each tile's row scale). */
 template <int FMT, int NT>
 struct MmaUnit {
-    static constexpr int SL = MmaStep<FMT>::SLABS;
-    static constexpr int WC = (FMT == FMT_Q4 || FMT == FMT_I8) ? 1 : 4;   /* 16-byte chunks per tile */
+    static constexpr int J = MmaStep<FMT>::J, SL = MmaStep<FMT>::SLABS;
+    static constexpr int NS = FMT == FMT_Q4 ? 4 : 1;
     u32x4 x[SL];
-    u32x4 w[NT][WC];
-    uint32_t s[NT][2];
+    u32x4 w[NT][J];
+    uint32_t s[NT][NS];
 };
+
+/* Byte offset of slab s's eight activations within a step, past the lane group's own offset
+   (16 g, or 32 g for int8): 16-bit and q4 slab s covers weights 32 s .. 32 s + 31 of the step
+   (q4: one block), int8 slab s half s % 2 of chunk s / 2. */
+template <int FMT>
+constexpr int mma_x_byte(int s) { return FMT == FMT_I8 ? 128 * (s / 2) + 16 * (s % 2) : 64 * s; }
 
 __device__ __forceinline__ u32x4 keep_if(bool ok, u32x4 v) { return ok ? v : zero4(); }
 
+/* A wave-uniform pointer held in scalar registers, so that a load from it plus a 32-bit lane
+   offset and a constant takes the scalar-base form (no per-lane address arithmetic). */
+__device__ __forceinline__ const char* uniform_ptr(const char* p) {
+    const uint64_t v = reinterpret_cast<uint64_t>(p);
+    const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return reinterpret_cast<const char*>(hi << 32 | lo);
+}
+
 /* Rows [r0, r1) of matrix d for tokens token0 .. token0 + ntok - 1 (ntok <= 16), NT tiles of 16
    rows per group.  The units (group, step) run as a two-set register pipeline, as in rows_q4: the
-   loads of the next unit are in flight while the current one is multiplied.  Every load is
-   unconditional with its address clamped into the operand: rows past r1 read row r1 - 1 and are
-   not stored, token slots past ntok read the first token and are not stored, and the values past
-   the row's end are zeroed when the ragged last step of K is multiplied (masking them as they
-   arrive would make each load wait at once).  q4 reads the four block scales of a step as one
-   8-byte load where the rows hold a multiple of 4 blocks and the scales are 8-byte aligned
-   (SCALE8); otherwise it reads them one by one. */
-template <int FMT, int NT, bool SCALE8>
+   loads of the next unit are in flight while the current one is multiplied.  Each load adds a
+   32-bit lane offset and a constant to a wave-uniform base, so it costs no vector arithmetic; the
+   lane offsets are set once per group, with rows past r1 clamped to row r1 - 1 (read, never
+   stored), and token slots past ntok read the first token (never stored).  Where a row's length
+   is not a whole number of steps, its last step is moved back to end at the row's end and the
+   values the previous step already covered are zeroed when it is multiplied (masking them as they
+   arrive would make each load wait at once).  Rows shorter than one step (SHORT) clamp each
+   lane's offset instead.  q4 reads a step's eight block scales as one 16-byte load where the rows
+   hold a multiple of 8 blocks and the scales are 16-byte aligned (SCALE16); otherwise one by one.
+   The caller keeps 16 NT rows of codes and 16 tokens of activations within 2^31 bytes. */
+template <int FMT, int NT, bool SCALE16, bool SHORT>
 __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1, int32_t token0, int ntok, int lane) {
     using Unit = MmaUnit<FMT, NT>;
-    constexpr int SK = MmaStep<FMT>::K, SL = Unit::SL, WC = Unit::WC;
-    const int c = lane & 15, g = lane >> 4;                      /* token slot and tile row; group  */
-    g_u32x4* x = as_global<g_u32x4*>(static_cast<const char*>(d.x) + (int64_t)(token0 + (c < ntok ? c : 0)) * d.x_stride);
-    g_u32x4* Wq = as_global<g_u32x4*>(d.w);
-    g_u16* S = as_global<g_u16*>(d.s);
-    const int64_t nc = d.nc;                                     /* blocks (q4) or 16-byte chunks    */
+    constexpr int J = Unit::J, SL = Unit::SL, SK = MmaStep<FMT>::K, SB = 64 * J;   /* SB: row bytes per step */
+    constexpr int XG = FMT == FMT_I8 ? 32 : 16;                  /* x bytes per lane group within a step */
+    const int c = lane & 15, g = lane >> 4;                      /* token slot and tile row; group       */
+    const int64_t nc = d.nc;                                     /* blocks (q4) or 16-byte chunks        */
+    const int64_t crb = nc * 16;                                 /* code (or weight) bytes per row       */
     const int64_t kelem = FMT == FMT_Q4 ? nc * 32 : FMT == FMT_I8 ? nc * 16 : nc * 8;
-    const int64_t steps = (kelem + SK - 1) / SK;
+    const int32_t steps = (int32_t)((crb + SB - 1) / SB);       /* at most 2^19 (rows up to 32 MiB) */
     const int64_t ngroups = (r1 - r0 + 16 * NT - 1) / (16 * NT);
     const int64_t n = ngroups * steps;                           /* units */
     if (n == 0) return;
+    const char* xb = static_cast<const char*>(d.x) + (int64_t)token0 * d.x_stride;   /* uniform */
+    const uint32_t vx = (uint32_t)((c < ntok ? c : 0) * d.x_stride) + XG * g;
+    const int64_t srow = FMT == FMT_Q4 ? nc * 2 : 2;             /* scale bytes per row */
     f4_t acc[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[t] = f4_t{0.f, 0.f, 0.f, 0.f};
-    int64_t gl = 0, kl = 0;                                      /* next unit to load     */
-    int64_t gc = 0, kc = 0;                                      /* next unit to multiply */
+    int64_t gl = 0, gc = 0;                                      /* group of the next unit to load, multiply */
+    int32_t kl = 0, kc = 0;                                      /* and its step                             */
+    const char* wg = nullptr;                                    /* this group's row r0 of codes, scales */
+    const char* sg = nullptr;
+    uint32_t vr[NT], vs[NT];                                     /* lane offsets: row of each tile */
     auto load = [&](Unit& u) {
-        const int64_t i0 = r0 + gl * 16 * NT, k0 = kl * SK;
+        if (kl == 0) {
+            const int64_t i0 = r0 + gl * 16 * NT;
+            wg = static_cast<const char*>(d.w) + i0 * crb;
+            sg = static_cast<const char*>(d.s) + i0 * srow;
 #pragma unroll
-        for (int j = 0; j < SL; ++j) {
-            const int64_t ke = FMT == FMT_I8 ? k0 + 16 * g + 8 * j : k0 + 32 * j + 8 * g;
-            u.x[j] = load_reused(x + std::min<int64_t>(ke, kelem - 8) / 8);
+            for (int t = 0; t < NT; ++t) {
+                const int64_t rr = std::min<int64_t>(i0 + 16 * t + c, r1 - 1) - i0;
+                vr[t] = (uint32_t)(rr * crb);
+                vs[t] = (uint32_t)(rr * srow);
+            }
+        }
+        if constexpr (!SHORT) {
+            const int64_t kb = std::min<int64_t>((int64_t)kl * SB, crb - SB);   /* the last step ends at the row's end */
+            const char* ws = uniform_ptr(wg + kb);
+            const char* xs = uniform_ptr(xb + std::min<int64_t>((int64_t)kl * SK, kelem - SK) * 2);
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int jj = 0; jj < J; ++jj)
+                    u.w[t][jj] = load_once(as_global<g_u32x4*>(ws + (vr[t] + 16 * g) + 64 * jj));
+#pragma unroll
+            for (int s = 0; s < SL; ++s) u.x[s] = load_reused(as_global<g_u32x4*>(xs + vx + mma_x_byte<FMT>(s)));
+        } else {                                                 /* one step, shorter than SB: clamp per lane */
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int jj = 0; jj < J; ++jj) {
+                    const uint32_t o = (uint32_t)std::min<int64_t>(64 * jj + 16 * g, crb - 16);
+                    u.w[t][jj] = load_once(as_global<g_u32x4*>(uniform_ptr(wg) + (vr[t] + o)));
+                }
+#pragma unroll
+            for (int s = 0; s < SL; ++s) {
+                const int64_t e = std::min<int64_t>((XG * g + mma_x_byte<FMT>(s)) / 2, kelem - 8);
+                u.x[s] = load_reused(as_global<g_u32x4*>(uniform_ptr(xb) + (vx - XG * g + (uint32_t)(2 * e))));
+            }
         }
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            const int64_t row = std::min<int64_t>(i0 + 16 * t + c, r1 - 1);
             if constexpr (FMT == FMT_Q4) {
-                const int64_t b = k0 / 32 + g;                   /* this group's block */
-                u.w[t][0] = load_once(Wq + row * nc + std::min<int64_t>(b, nc - 1));
-                const int64_t b0 = k0 / 32;
-                if constexpr (SCALE8) {
-                    const uint64_t v = *reinterpret_cast<__attribute__((address_space(1))) const uint64_t*>(S + row * nc + b0);
-                    u.s[t][0] = (uint32_t)v;
-                    u.s[t][1] = (uint32_t)(v >> 32);
+                const int64_t b0 = SHORT ? 0 : std::min<int64_t>((int64_t)kl * 8, nc - 8);   /* the step's first block */
+                if constexpr (SCALE16) {
+                    const u32x4 v = load_reused(as_global<g_u32x4*>(uniform_ptr(sg + b0 * 2) + vs[t]));
+                    u.s[t][0] = v.x, u.s[t][1] = v.y, u.s[t][2] = v.z, u.s[t][3] = v.w;
                 } else {
-                    uint32_t h[4];
+                    uint32_t h[8];
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) h[j] = S[row * nc + std::min<int64_t>(b0 + j, nc - 1)];
-                    u.s[t][0] = h[0] | h[1] << 16;
-                    u.s[t][1] = h[2] | h[3] << 16;
+                    for (int j = 0; j < 8; ++j)
+                        h[j] = *as_global<g_u16*>(uniform_ptr(sg + std::min<int64_t>(b0 + j, nc - 1) * 2) + vs[t]);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) u.s[t][j] = h[2 * j] | h[2 * j + 1] << 16;
                 }
             } else if constexpr (FMT == FMT_I8) {
-                const int64_t ch = k0 / 16 + g;
-                u.w[t][0] = load_once(Wq + row * nc + std::min<int64_t>(ch, nc - 1));
-                u.s[t][0] = S[row];
-            } else {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int64_t ke = k0 + 32 * j + 8 * g;
-                    u.w[t][j] = load_once(Wq + row * nc + std::min<int64_t>(ke, kelem - 8) / 8);
-                }
+                u.s[t][0] = *as_global<g_u16*>(uniform_ptr(sg) + vs[t]);
             }
         }
         if (++kl == steps) { kl = 0; ++gl; }
     };
     auto multiply = [&](Unit& u) {
-        const int64_t i0 = r0 + gc * 16 * NT, k0 = kc * SK;
-        if (k0 + SK > kelem) {                                   /* the ragged last step of K */
+        const int64_t i0 = r0 + gc * 16 * NT;
+        /* the step's first weight, and the first one it has not already covered */
+        const int64_t e0 = SHORT ? 0 : std::min<int64_t>((int64_t)kc * SK, kelem - SK), e1 = SHORT ? 0 : (int64_t)kc * SK;
+        if (SHORT || e0 < e1) {                                  /* a moved-back or short last step */
 #pragma unroll
-            for (int j = 0; j < SL; ++j) {
-                const int64_t ke = FMT == FMT_I8 ? k0 + 16 * g + 8 * j : k0 + 32 * j + 8 * g;
-                u.x[j] = keep_if(ke < kelem, u.x[j]);
-                if constexpr (WC == 4) {
+            for (int s = 0; s < SL; ++s) {
+                const int64_t e = e0 + (XG * g + mma_x_byte<FMT>(s)) / 2;
+                u.x[s] = keep_if(e >= e1 && e < kelem, u.x[s]);
+            }
+            if constexpr (FMT != FMT_Q4 && FMT != FMT_I8) {     /* 16-bit weights there may not be finite */
 #pragma unroll
-                    for (int t = 0; t < NT; ++t) u.w[t][j] = keep_if(ke < kelem, u.w[t][j]);
-                }
+                for (int t = 0; t < NT; ++t)
+#pragma unroll
+                    for (int jj = 0; jj < J; ++jj) {
+                        const int64_t e = e0 + 32 * jj + 8 * g;
+                        u.w[t][jj] = keep_if(e >= e1 && e < kelem, u.w[t][jj]);
+                    }
             }
         }
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             if constexpr (FMT == FMT_Q4) {
-                const u32x4 w = transpose_groups(u.w[t][0]);
-                const uint32_t wj[4] = {w.x, w.y, w.z, w.w};
-                const uint16_t sh[4] = {(uint16_t)u.s[t][0], (uint16_t)(u.s[t][0] >> 16), (uint16_t)u.s[t][1],
-                                        (uint16_t)(u.s[t][1] >> 16)};
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const float sc = k0 / 32 + j < nc ? f16_bits_to_f32(sh[j]) : 0.f;
-                    const f4_t p = mma16<FMT_F16>(x8_q4_order(u.x[j]), q4_word_f16(wj[j]), f4_t{0.f, 0.f, 0.f, 0.f});
-                    acc[t] += sc * p;
+                for (int jj = 0; jj < J; ++jj) {
+                    const u32x4 w = transpose_groups(u.w[t][jj]);
+                    const uint32_t wj[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {                /* block e0 / 32 + s of the row */
+                        const int s = 4 * jj + j;
+                        float sc = f16_bits_to_f32((uint16_t)(u.s[t][s / 2] >> (16 * (s % 2))));
+                        if constexpr (!SCALE16) {                /* blocks outside the step's new part */
+                            const int64_t b = e0 / 32 + s;
+                            sc = b >= e1 / 32 && b < nc ? sc : 0.f;
+                        }
+                        const f4_t p = mma16<FMT_F16>(x8_q4_order(u.x[s]), q4_word_f16(wj[j]), f4_t{0.f, 0.f, 0.f, 0.f});
+                        acc[t] += sc * p;
+                    }
                 }
             } else if constexpr (FMT == FMT_I8) {
-                acc[t] = mma16<FMT_F16>(x8_i8_order(u.x[0]), i8_words_f16(u.w[t][0].x, u.w[t][0].y), acc[t]);
-                acc[t] = mma16<FMT_F16>(x8_i8_order(u.x[1]), i8_words_f16(u.w[t][0].z, u.w[t][0].w), acc[t]);
+#pragma unroll
+                for (int jj = 0; jj < J; ++jj) {
+                    acc[t] = mma16<FMT_F16>(x8_i8_order(u.x[2 * jj]), i8_words_f16(u.w[t][jj].x, u.w[t][jj].y), acc[t]);
+                    acc[t] = mma16<FMT_F16>(x8_i8_order(u.x[2 * jj + 1]), i8_words_f16(u.w[t][jj].z, u.w[t][jj].w), acc[t]);
+                }
             } else {
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[t] = mma16<FMT>(u.x[j], u.w[t][j], acc[t]);
+                for (int jj = 0; jj < J; ++jj) acc[t] = mma16<FMT>(u.x[jj], u.w[t][jj], acc[t]);
             }
         }
         if (kc + 1 == steps) {                                   /* end of a group: store, reset */
@@ -1186,15 +1249,20 @@ __device__ __forceinline__ void stream_range_mma(const DevMat* __restrict__ tab,
         const int fmt = FMT ? FMT : d.fmt;
         const RowRange rr = range_rows(d, lo, hi, 16 * NT);
         if (rr.r0 >= rr.r1) continue;
-        if ((FMT == 0 || FMT == FMT_F16) && fmt == FMT_F16)
-            rows_mma<FMT_F16, NT, false>(d, rr.r0, rr.r1, token0, ntok, lane);
-        else if ((FMT == 0 || FMT == FMT_BF16) && fmt == FMT_BF16)
-            rows_mma<FMT_BF16, NT, false>(d, rr.r0, rr.r1, token0, ntok, lane);
-        else if ((FMT == 0 || FMT == FMT_Q4) && fmt == FMT_Q4) {
-            if (d.nc % 4 == 0 && (reinterpret_cast<uintptr_t>(d.s) & 7) == 0) rows_mma<FMT_Q4, NT, true>(d, rr.r0, rr.r1, token0, ntok, lane);
-            else rows_mma<FMT_Q4, NT, false>(d, rr.r0, rr.r1, token0, ntok, lane);
-        } else if ((FMT == 0 || FMT == FMT_I8) && fmt == FMT_I8)
-            rows_mma<FMT_I8, NT, false>(d, rr.r0, rr.r1, token0, ntok, lane);
+        const bool short_rows = d.nc * 16 < 64 * (fmt == FMT_Q4 || fmt == FMT_I8 ? 2 : 4);   /* under one step */
+#define WSR_ROWS(F, S16, SH) rows_mma<F, NT, S16, SH>(d, rr.r0, rr.r1, token0, ntok, lane)
+        if ((FMT == 0 || FMT == FMT_F16) && fmt == FMT_F16) {
+            if (short_rows) WSR_ROWS(FMT_F16, false, true); else WSR_ROWS(FMT_F16, false, false);
+        } else if ((FMT == 0 || FMT == FMT_BF16) && fmt == FMT_BF16) {
+            if (short_rows) WSR_ROWS(FMT_BF16, false, true); else WSR_ROWS(FMT_BF16, false, false);
+        } else if ((FMT == 0 || FMT == FMT_Q4) && fmt == FMT_Q4) {
+            if (short_rows) WSR_ROWS(FMT_Q4, false, true);
+            else if (d.nc % 8 == 0 && (reinterpret_cast<uintptr_t>(d.s) & 15) == 0) WSR_ROWS(FMT_Q4, true, false);
+            else WSR_ROWS(FMT_Q4, false, false);
+        } else if ((FMT == 0 || FMT == FMT_I8) && fmt == FMT_I8) {
+            if (short_rows) WSR_ROWS(FMT_I8, false, true); else WSR_ROWS(FMT_I8, false, false);
+        }
+#undef WSR_ROWS
     }
 }
 

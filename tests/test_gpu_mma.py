@@ -137,3 +137,38 @@ def test_mma_full_size(name):
             assert rel_l2(got, np.array(want)) <= TOL, (m.name, m.layer, t)
     del inp, valu, mma
     torch.cuda.empty_cache()
+
+
+# rows shorter than one step of K (one clamped step), and a q4 shape whose scales load 8 at a time
+SHORT = [(wl.F16, 33, 40), (wl.BF16, 20, 120), (wl.Q4, 40, 96), (wl.I8, 50, 48), (wl.I8, 17, 16),
+         (wl.Q4, 70, 4096)]
+
+
+@pytest.mark.parametrize("fmt,M,K", SHORT, ids=lambda v: str(v))
+@pytest.mark.parametrize("T", [1, 7, 16])
+def test_mma_short_rows_parity_and_bounds(fmt, M, K, T):
+    W, S = host_matrix(fmt, M, K, seed=9)
+    xfmt = wl.BF16 if fmt == wl.BF16 else wl.F16
+    X = synth.normal16((T + 1, K), wl.X_SIGMA, xfmt, seed=9, stream=604)
+    y = run_mma(fmt, W, S, X, M, K, T, y_rows=M + 3)
+    assert np.isnan(y[:, M:]).all() and np.isnan(y[T:]).all()
+    ora = oracle.get()
+    for t in range(T):
+        want = ora.gemv(dict(fmt=fmt, w=W, s=S), X[t]) if fmt in (wl.Q4, wl.I8) else ora.gemv16(W, X[t], fmt)
+        assert rel_l2(y[t, :M], want) <= TOL, (fmt, t)
+
+
+@pytest.mark.parametrize("fmt,M,K", SHORT, ids=lambda v: str(v))
+def test_mma_short_rows_unit_vectors_exact(fmt, M, K):
+    W, S = host_matrix(fmt, M, K, seed=10)
+    xfmt = wl.BF16 if fmt == wl.BF16 else wl.F16
+    zero, one = synth.encode16([0.0, 1.0], xfmt)
+    cols = sorted({0, 1, 7, 8, K // 2, K - 9, K - 1} & set(range(K)))[:16]
+    X = np.full((len(cols), K), zero, np.uint16)
+    for t, j in enumerate(cols):
+        X[t, j] = one
+    y = run_mma(fmt, W, S, X, M, K, len(cols))
+    ora = oracle.get()
+    for t, j in enumerate(cols):
+        want = ora.gemv(dict(fmt=fmt, w=W, s=S), X[t]) if fmt in (wl.Q4, wl.I8) else ora.gemv16(W, X[t], fmt)
+        assert np.array_equal(f32_bits(y[t]), f32_bits(want)), (fmt, j)
