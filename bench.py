@@ -5,6 +5,8 @@ Headline: the batch-1 decode weight sweep of a synthetic Llama-70B-shaped model 
 d 8192, 64 q / 8 kv heads of dim 128, FFN 28672, vocab 128256; 139.0 GB of weights read per token),
 fully HBM-resident; one step = one decode token = one persistent launch over every matrix.
 `value` is the achieved weight-read rate in GB/s (decimal), counting each weight byte once.
+The headline and q4 sweeps (and the protocol) also report the same tokens batched b per weight
+pass, on the vector ALUs (bit-identical outputs) and on the matrix cores (b <= 16, within rounding).
 
 Also measured in the same run and reported under "rows" (same JSON line):
   probe        pure-read reference, 1 GiB fp32 -> fp64 sum, HBM-resident and host-mapped
@@ -163,6 +165,7 @@ def run_sweep(name, steps, warmup, stream, wsr, want_cpu, cpu_seconds, passes=4)
            "launches_per_token": 1, "parity": parity, "passes": spread(pass_ms)}
     if batched is not None:
         out["batched"] = batched
+    out["batched_matrix_cores"] = mma_sweep(name, inp, specs, ws, steps, bpt, stream, wsr)
     if want_cpu:
         out["cpu_baseline"] = cpu_baseline(inp, bpt, cpu_seconds)
     del specs, ws, inp
@@ -190,6 +193,34 @@ def batch_sweep(name, inp, specs, ws, steps, bpt, stream, wsr, batches=(1, 2, 4,
                     "bitwise_equal_to_token_by_token": bool(same)})
         log(f"{name}: batch {b:2d}: {steps / sec:8.2f} tok/s, HBM {passes * bpt / sec / 1e9:7.1f} GB/s, "
             f"logical weight rate {steps * bpt / sec / 1e9:8.1f} GB/s, same outputs: {same}")
+    del ref
+    return res
+
+
+def mma_sweep(name, inp, specs, ws, steps, bpt, stream, wsr, batches=(1, 2, 4, 8, 16)):
+    """Batched decode on the matrix cores: b tokens share one pass over the weights (b <= 16).
+    The outputs agree with the token-by-token sweep within rounding; the worst rel-L2 is reported."""
+    import torch
+    ref = [y.clone() for y in inp.y]           # the token-by-token outputs
+    res = []
+    for b in batches:
+        if b > steps:
+            break
+        run = lambda: wsr.wsr_decode_sweep_mma(specs, b, ws, ws.numel(), stream)
+        run()
+        torch.cuda.synchronize()
+        worst = 0.0
+        for a, y in zip(ref, inp.y):
+            d = torch.linalg.vector_norm((y[:b] - a[:b]).double(), dim=1)
+            n = torch.linalg.vector_norm(a[:b].double(), dim=1).clamp_min(1e-30)
+            worst = max(worst, float((d / n).max()))
+        sec = median_of(run, 1, 5, stream)
+        res.append({"batch": b, "ms_per_pass": sec * 1e3, "tokens_per_s": b / sec, "hbm_GBps": bpt / sec / 1e9,
+                    "logical_weight_GBps": b * bpt / sec / 1e9, "worst_rel_l2_vs_token_by_token": worst})
+        log(f"{name}: matrix cores, batch {b:2d}: {b / sec:8.2f} tok/s, HBM {bpt / sec / 1e9:7.1f} GB/s, "
+            f"worst rel-L2 vs token by token {worst:.1e}")
+    for a, y in zip(ref, inp.y):               # leave the token-by-token outputs in place
+        y.copy_(a)
     del ref
     return res
 
@@ -331,7 +362,7 @@ def row_gemv_f16(stream, wsr):
     return res
 
 
-def row_protocol(stream, wsr, warmup_passes=12, passes=31, tokens=8):
+def row_protocol(stream, wsr, warmup_passes=12, passes=31, tokens=16):
     """The matched protocol of Sec. 3.1: a pass is one single-token int8 GEMV (fp16 row scales) over
     each of 12 distinct 12288 x 7168 matrices, bracketed by one synchronisation; the first 12
     passes are discarded and the median pass is reported, counting weight bytes once.  Measured as
@@ -370,6 +401,7 @@ def row_protocol(stream, wsr, warmup_passes=12, passes=31, tokens=8):
     res["parity"] = check_sweep(inp, [0, tokens - 1], nrows=4)
     log(f"protocol: parity on sampled rows: worst rel-L2 {res['parity']['worst_rel_l2']:.2e}")
     res["batched"] = batch_sweep("protocol", inp, specs, ws, tokens, nbytes, stream, wsr, (1, 2, 4, 8))
+    res["batched_matrix_cores"] = mma_sweep("protocol", inp, specs, ws, tokens, nbytes, stream, wsr)
     del specs, ws, inp
     torch.cuda.empty_cache()
     return res
