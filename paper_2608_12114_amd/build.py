@@ -61,20 +61,26 @@ def _run(cmd):
     return r
 
 
+KERNEL_FILES = ("wsr_kernels.hip", "wsr_mma.hip")
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(OUT_DIR, exist_ok=True)
-    k_obj = os.path.join(OUT_DIR, "wsr_kernels.o")
+    objs = []
+    for src in KERNEL_FILES:
+        obj = os.path.join(OUT_DIR, src.replace(".hip", ".o"))
+        r = _run(["hipcc", *COMMON, *DEVICE, *_MIR_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        if "IR Dump Before" not in r.stderr:
+            raise RuntimeError(f"build: the compiler printed no machine code for the peephole check ({src})")
+        dropped = dropped_live_scc(r.stderr)
+        if dropped:
+            raise RuntimeError(f"build: the pre-emit peephole removed live SCC definitions in {src} "
+                               "(miscompiled selects):\n  " + "\n  ".join(dropped))
+        objs.append(obj)
     a_obj = os.path.join(OUT_DIR, "wsr_api.o")
-    r = _run(["hipcc", *COMMON, *DEVICE, *_MIR_FLAGS, "-c", os.path.join(CSRC, "wsr_kernels.hip"), "-o", k_obj])
-    if "IR Dump Before" not in r.stderr:
-        raise RuntimeError("build: the compiler printed no machine code for the peephole check")
-    dropped = dropped_live_scc(r.stderr)
-    if dropped:
-        raise RuntimeError("build: the pre-emit peephole removed live SCC definitions (miscompiled "
-                           "selects):\n  " + "\n  ".join(dropped))
     _run(["hipcc", *COMMON, "-c", os.path.join(CSRC, "wsr_api.cpp"), "-o", a_obj])
     tmp = LIB_PATH + ".tmp"
-    _run(["hipcc", "-shared", "-fPIC", f"--offload-arch={ARCH}", k_obj, a_obj, "-o", tmp])
+    _run(["hipcc", "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, a_obj, "-o", tmp])
     os.replace(tmp, LIB_PATH)
     if verbose:
         print("built", LIB_PATH)

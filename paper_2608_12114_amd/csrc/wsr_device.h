@@ -887,17 +887,6 @@ __device__ __forceinline__ int first_matrix(const int64_t* __restrict__ cost, in
     return a;
 }
 
-/* Rows [r0, r1) of matrix d that the byte range [lo, hi) of the weight stream covers.  A byte
-   boundary maps to the first group of g rows starting at or after it, the same way for the ranges
-   on both sides, so the ranges still cover each row once and break only between whole groups. */
-struct RowRange {
-    int64_t r0, r1;
-};
-__device__ __forceinline__ RowRange range_rows(const DevMat& d, int64_t lo, int64_t hi, int64_t g) {
-    const int64_t r0 = lo > d.cost0 ? ceil_div(lo - d.cost0, d.row_bytes * g) * g : 0;
-    const int64_t e1 = ceil_div(hi - d.cost0, d.row_bytes * g) * g;
-    return RowRange{r0, d.M < e1 ? d.M : e1};
-}
 
 template <int FMT, int R16, int U16, int RQ, int UQ, int QNB = 2, int T = 1, int RC = Cols16<T>::R,
           int UC = Cols16<T>::U, int RQC = Cols4<(T <= 8 ? T : 8)>::R>
@@ -912,7 +901,7 @@ __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, con
         const int64_t g = fmt == FMT_Q4 ? (T == 1 ? RQ : RQC)
                         : fmt == FMT_I8 ? ColsI8<(T <= 8 ? T : 8)>::R
                                         : (T == 1 ? R16 : RC);
-        /* range_rows' mapping, written out here: as a call it changes this loop's code. */
+        /* a byte range maps to rows by rounding both ends up to the next group of g rows */
         const int64_t r0 = lo > d.cost0 ? ceil_div(lo - d.cost0, d.row_bytes * g) * g : 0;
         const int64_t e1 = ceil_div(hi - d.cost0, d.row_bytes * g) * g;
         const int64_t r1 = d.M < e1 ? d.M : e1;
@@ -936,333 +925,6 @@ __device__ __forceinline__ void stream_range(const DevMat* __restrict__ tab, con
                 else if ((FMT == 0 || FMT == FMT_I8) && fmt == FMT_I8) rows_i8<T>(d, r0, r1, token, lane);
             }
         }
-    }
-}
-
-/* ---- matrix-core rows: up to 16 tokens per pass over the weights ----------------------------------
-
-   With several tokens per pass the packed dot products of the loops above cost one instruction per
-   weight pair per token, and from about four tokens on the vector ALUs, not HBM, set the rate.
-   These loops hand the products to the matrix cores instead.  A wave owns tiles of 16 rows; per
-   32-element slab of K it forms D = X^T W^T for the tile with one v_mfma_f32_16x16x32: the A
-   operand holds 16 token columns of activations (columns past the pass's tokens are zero), the B
-   operand 16 weight rows decoded to fp16.  Decoded weights are exact: q4 and int8 codes become the
-   small integers q as 1024 + (q + bias) formed by one bit operation, minus 1024 + bias by one packed
-   fp16 subtraction; 16-bit weights are used as stored.  Every product q x is exact in fp32, and
-   the scales multiply the fp32 slab sums, but the matrix core adds a slab's products in an order of
-   its own, so these results agree with the other loops within rounding, not bit for bit.
-   Operand layout (checked on the device): lane i holds A[i%16][8(i/16)+j], B[8(i/16)+j][i%16] and
-   D[4(i/16)+j][i%16].  K may be permuted inside a slab as long as A and B follow the same order;
-   the decoders give (k0,k4,k1,k5,k2,k6,k3,k7) for a q4 word and (k0,k2,k1,k3,k4,k6,k5,k7) for two
-   int8 words, and the activation loaders permute x to match.  A q4 scale covers one block of 32, so
-   a slab is one block: the four words a lane loaded (block b0 + i/16 of row i%16) are transposed
-   between the four 16-lane groups with two rounds of lane swaps, and each block's product is formed
-   alone and added with its row's scale.  int8 scales are per row and multiply the finished sum. */
-typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
-typedef __bf16 b8_t __attribute__((ext_vector_type(8)));
-typedef float f4_t __attribute__((ext_vector_type(4)));
-
-constexpr int MMA_TOKENS = 16;              /* token columns per tile                               */
-
-template <int FMT>
-__device__ __forceinline__ f4_t mma16(u32x4 a, u32x4 b, f4_t c) {
-    if constexpr (FMT == FMT_BF16)
-        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(b8_t, a), __builtin_bit_cast(b8_t, b), c,
-                                                       0, 0, 0);
-    else
-        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, a), __builtin_bit_cast(h8_t, b), c,
-                                                      0, 0, 0);
-}
-
-/* v - bias in both fp16 halves of a word holding 1024 + v (exact for the small integers here). */
-__device__ __forceinline__ uint32_t f16_sub_bias(uint32_t v, uint32_t neg_bias) {
-    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(h2_t, v) + __builtin_bit_cast(h2_t, neg_bias));
-}
-
-/* One q4 code word (code k in nibble k) as 8 fp16 integers, order (k0,k4,k1,k5,k2,k6,k3,k7). */
-__device__ __forceinline__ u32x4 q4_word_f16(uint32_t w) {
-    constexpr uint32_t M = 0x000F000Fu, E = 0x64086408u, NEG = 0xE408E408u;   /* 1024 + (code ^ 8); -1032 */
-    return u32x4{f16_sub_bias((w & M) ^ E, NEG), f16_sub_bias(((w >> 4) & M) ^ E, NEG),
-                 f16_sub_bias(((w >> 8) & M) ^ E, NEG), f16_sub_bias(((w >> 12) & M) ^ E, NEG)};
-}
-
-/* Two int8 code words (codes k0..k3, k4..k7) as 8 fp16 integers, order (k0,k2,k1,k3,k4,k6,k5,k7). */
-__device__ __forceinline__ u32x4 i8_words_f16(uint32_t w0, uint32_t w1) {
-    constexpr uint32_t M = 0x00FF00FFu, E = 0x64806480u, NEG = 0xE480E480u;   /* 1024 + (code ^ 128); -1152 */
-    return u32x4{f16_sub_bias((w0 & M) ^ E, NEG), f16_sub_bias(((w0 >> 8) & M) ^ E, NEG),
-                 f16_sub_bias((w1 & M) ^ E, NEG), f16_sub_bias(((w1 >> 8) & M) ^ E, NEG)};
-}
-
-/* Eight activations x0..x7 (16 bytes) in the q4 decoder's order and in the int8 decoder's order. */
-__device__ __forceinline__ u32x4 x8_q4_order(u32x4 u) {
-    return u32x4{__builtin_amdgcn_perm(u.z, u.x, 0x05040100u), __builtin_amdgcn_perm(u.z, u.x, 0x07060302u),
-                 __builtin_amdgcn_perm(u.w, u.y, 0x05040100u), __builtin_amdgcn_perm(u.w, u.y, 0x07060302u)};
-}
-__device__ __forceinline__ u32x4 x8_i8_order(u32x4 u) {
-    return u32x4{__builtin_amdgcn_perm(u.y, u.x, 0x05040100u), __builtin_amdgcn_perm(u.y, u.x, 0x07060302u),
-                 __builtin_amdgcn_perm(u.w, u.z, 0x05040100u), __builtin_amdgcn_perm(u.w, u.z, 0x07060302u)};
-}
-
-/* Lane group g (lanes 16g .. 16g + 15) holds the four words of block g in w; afterwards it holds
-   word g of blocks 0, 1, 2, 3 in w.x, w.y, w.z, w.w (a 4 x 4 transpose between the groups). */
-__device__ __forceinline__ u32x4 transpose_groups(u32x4 w) {
-    const auto s02 = __builtin_amdgcn_permlane32_swap(w.x, w.z, false, false);
-    const auto s13 = __builtin_amdgcn_permlane32_swap(w.y, w.w, false, false);
-    const auto s01 = __builtin_amdgcn_permlane16_swap(s02[0], s13[0], false, false);
-    const auto s23 = __builtin_amdgcn_permlane16_swap(s02[1], s13[1], false, false);
-    return u32x4{s01[0], s01[1], s23[0], s23[1]};
-}
-
-/* One step of the matrix-core loops.  Each lane reads J 16-byte chunks of its row per tile, chunk
-   jj of lane group g at byte 64 jj + 16 g of the step, so a load instruction covers 64 contiguous
-   bytes of each of 16 rows and a step 64 J bytes of every row.  HBM delivers about half its rate
-   when a wave reads only 64 bytes of a row per step, so q4 and int8 take two chunks.  SLABS is the
-   number of matrix instructions per tile and step, K the weights per row and step. */
-template <int FMT> struct MmaStep { static constexpr int J = 4, SLABS = 4, K = 128; };    /* 8 per chunk   */
-template <> struct MmaStep<FMT_Q4> { static constexpr int J = 2, SLABS = 8, K = 256; };   /* 32 per chunk  */
-template <> struct MmaStep<FMT_I8> { static constexpr int J = 2, SLABS = 4, K = 128; };   /* 16 per chunk  */
-
-/* Registers of one unit (a group of NT tiles, one step): the activations of each slab, the chunks
-   of each tile, and the scales (q4: the step's eight block scales of each tile's row, as fp16
-   pairs; int8: each tile's row scale). */
-template <int FMT, int NT>
-struct MmaUnit {
-    static constexpr int J = MmaStep<FMT>::J, SL = MmaStep<FMT>::SLABS;
-    static constexpr int NS = FMT == FMT_Q4 ? 4 : 1;
-    u32x4 x[SL];
-    u32x4 w[NT][J];
-    uint32_t s[NT][NS];
-};
-
-/* Byte offset of slab s's eight activations within a step, past the lane group's own offset
-   (16 g, or 32 g for int8): 16-bit and q4 slab s covers weights 32 s .. 32 s + 31 of the step
-   (q4: one block), int8 slab s half s % 2 of chunk s / 2. */
-template <int FMT>
-constexpr int mma_x_byte(int s) { return FMT == FMT_I8 ? 128 * (s / 2) + 16 * (s % 2) : 64 * s; }
-
-__device__ __forceinline__ u32x4 keep_if(bool ok, u32x4 v) { return ok ? v : zero4(); }
-
-/* A wave-uniform pointer held in scalar registers, so that a load from it plus a 32-bit lane
-   offset and a constant takes the scalar-base form (no per-lane address arithmetic). */
-__device__ __forceinline__ const char* uniform_ptr(const char* p) {
-    const uint64_t v = reinterpret_cast<uint64_t>(p);
-    const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
-    const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
-    return reinterpret_cast<const char*>(hi << 32 | lo);
-}
-
-/* Rows [r0, r1) of matrix d for tokens token0 .. token0 + ntok - 1 (ntok <= 16), NT tiles of 16
-   rows per group.  The units (group, step) run as a two-set register pipeline, as in rows_q4: the
-   loads of the next unit are in flight while the current one is multiplied.  Each load adds a
-   32-bit lane offset and a constant to a wave-uniform base, so it costs no vector arithmetic; the
-   lane offsets are set once per group, with rows past r1 clamped to row r1 - 1 (read, never
-   stored), and token slots past ntok read the first token (never stored).  Where a row's length
-   is not a whole number of steps, its last step is moved back to end at the row's end and the
-   values the previous step already covered are zeroed when it is multiplied (masking them as they
-   arrive would make each load wait at once).  Rows shorter than one step (SHORT) clamp each
-   lane's offset instead.  q4 reads a step's eight block scales as one 16-byte load where the rows
-   hold a multiple of 8 blocks and the scales are 16-byte aligned (SCALE16); otherwise one by one.
-   The caller keeps 16 NT rows of codes and 16 tokens of activations within 2^31 bytes. */
-template <int FMT, int NT, bool SCALE16, bool SHORT>
-__device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1, int32_t token0, int ntok, int lane) {
-    using Unit = MmaUnit<FMT, NT>;
-    constexpr int J = Unit::J, SL = Unit::SL, SK = MmaStep<FMT>::K, SB = 64 * J;   /* SB: row bytes per step */
-    constexpr int XG = FMT == FMT_I8 ? 32 : 16;                  /* x bytes per lane group within a step */
-    const int c = lane & 15, g = lane >> 4;                      /* token slot and tile row; group       */
-    const int64_t nc = d.nc;                                     /* blocks (q4) or 16-byte chunks        */
-    const int64_t crb = nc * 16;                                 /* code (or weight) bytes per row       */
-    const int64_t kelem = FMT == FMT_Q4 ? nc * 32 : FMT == FMT_I8 ? nc * 16 : nc * 8;
-    const int32_t steps = (int32_t)((crb + SB - 1) / SB);       /* at most 2^19 (rows up to 32 MiB) */
-    const int64_t ngroups = (r1 - r0 + 16 * NT - 1) / (16 * NT);
-    const int64_t n = ngroups * steps;                           /* units */
-    if (n == 0) return;
-    const char* xb = static_cast<const char*>(d.x) + (int64_t)token0 * d.x_stride;   /* uniform */
-    const uint32_t vx = (uint32_t)((c < ntok ? c : 0) * d.x_stride) + XG * g;
-    const int64_t srow = FMT == FMT_Q4 ? nc * 2 : 2;             /* scale bytes per row */
-    f4_t acc[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) acc[t] = f4_t{0.f, 0.f, 0.f, 0.f};
-    int64_t gl = 0, gc = 0;                                      /* group of the next unit to load, multiply */
-    int32_t kl = 0, kc = 0;                                      /* and its step                             */
-    const char* wg = nullptr;                                    /* this group's row r0 of codes, scales */
-    const char* sg = nullptr;
-    uint32_t vr[NT], vs[NT];                                     /* lane offsets: row of each tile */
-    auto load = [&](Unit& u) {
-        if (kl == 0) {
-            const int64_t i0 = r0 + gl * 16 * NT;
-            wg = static_cast<const char*>(d.w) + i0 * crb;
-            sg = static_cast<const char*>(d.s) + i0 * srow;
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                const int64_t rr = std::min<int64_t>(i0 + 16 * t + c, r1 - 1) - i0;
-                vr[t] = (uint32_t)(rr * crb);
-                vs[t] = (uint32_t)(rr * srow);
-            }
-        }
-        if constexpr (!SHORT) {
-            const int64_t kb = std::min<int64_t>((int64_t)kl * SB, crb - SB);   /* the last step ends at the row's end */
-            const char* ws = uniform_ptr(wg + kb);
-            const char* xs = uniform_ptr(xb + std::min<int64_t>((int64_t)kl * SK, kelem - SK) * 2);
-#pragma unroll
-            for (int t = 0; t < NT; ++t)
-#pragma unroll
-                for (int jj = 0; jj < J; ++jj)
-                    u.w[t][jj] = load_once(as_global<g_u32x4*>(ws + (vr[t] + 16 * g) + 64 * jj));
-#pragma unroll
-            for (int s = 0; s < SL; ++s) u.x[s] = load_reused(as_global<g_u32x4*>(xs + vx + mma_x_byte<FMT>(s)));
-        } else {                                                 /* one step, shorter than SB: clamp per lane */
-#pragma unroll
-            for (int t = 0; t < NT; ++t)
-#pragma unroll
-                for (int jj = 0; jj < J; ++jj) {
-                    const uint32_t o = (uint32_t)std::min<int64_t>(64 * jj + 16 * g, crb - 16);
-                    u.w[t][jj] = load_once(as_global<g_u32x4*>(uniform_ptr(wg) + (vr[t] + o)));
-                }
-#pragma unroll
-            for (int s = 0; s < SL; ++s) {
-                const int64_t e = std::min<int64_t>((XG * g + mma_x_byte<FMT>(s)) / 2, kelem - 8);
-                u.x[s] = load_reused(as_global<g_u32x4*>(uniform_ptr(xb) + (vx - XG * g + (uint32_t)(2 * e))));
-            }
-        }
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            if constexpr (FMT == FMT_Q4) {
-                const int64_t b0 = SHORT ? 0 : std::min<int64_t>((int64_t)kl * 8, nc - 8);   /* the step's first block */
-                if constexpr (SCALE16) {
-                    const u32x4 v = load_reused(as_global<g_u32x4*>(uniform_ptr(sg + b0 * 2) + vs[t]));
-                    u.s[t][0] = v.x, u.s[t][1] = v.y, u.s[t][2] = v.z, u.s[t][3] = v.w;
-                } else {
-                    uint32_t h[8];
-#pragma unroll
-                    for (int j = 0; j < 8; ++j)
-                        h[j] = *as_global<g_u16*>(uniform_ptr(sg + std::min<int64_t>(b0 + j, nc - 1) * 2) + vs[t]);
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) u.s[t][j] = h[2 * j] | h[2 * j + 1] << 16;
-                }
-            } else if constexpr (FMT == FMT_I8) {
-                u.s[t][0] = *as_global<g_u16*>(uniform_ptr(sg) + vs[t]);
-            }
-        }
-        if (++kl == steps) { kl = 0; ++gl; }
-    };
-    auto multiply = [&](Unit& u) {
-        const int64_t i0 = r0 + gc * 16 * NT;
-        /* the step's first weight, and the first one it has not already covered */
-        const int64_t e0 = SHORT ? 0 : std::min<int64_t>((int64_t)kc * SK, kelem - SK), e1 = SHORT ? 0 : (int64_t)kc * SK;
-        if (SHORT || e0 < e1) {                                  /* a moved-back or short last step */
-#pragma unroll
-            for (int s = 0; s < SL; ++s) {
-                const int64_t e = e0 + (XG * g + mma_x_byte<FMT>(s)) / 2;
-                u.x[s] = keep_if(e >= e1 && e < kelem, u.x[s]);
-            }
-            if constexpr (FMT != FMT_Q4 && FMT != FMT_I8) {     /* 16-bit weights there may not be finite */
-#pragma unroll
-                for (int t = 0; t < NT; ++t)
-#pragma unroll
-                    for (int jj = 0; jj < J; ++jj) {
-                        const int64_t e = e0 + 32 * jj + 8 * g;
-                        u.w[t][jj] = keep_if(e >= e1 && e < kelem, u.w[t][jj]);
-                    }
-            }
-        }
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            if constexpr (FMT == FMT_Q4) {
-#pragma unroll
-                for (int jj = 0; jj < J; ++jj) {
-                    const u32x4 w = transpose_groups(u.w[t][jj]);
-                    const uint32_t wj[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {                /* block e0 / 32 + s of the row */
-                        const int s = 4 * jj + j;
-                        float sc = f16_bits_to_f32((uint16_t)(u.s[t][s / 2] >> (16 * (s % 2))));
-                        if constexpr (!SCALE16) {                /* blocks outside the step's new part */
-                            const int64_t b = e0 / 32 + s;
-                            sc = b >= e1 / 32 && b < nc ? sc : 0.f;
-                        }
-                        const f4_t p = mma16<FMT_F16>(x8_q4_order(u.x[s]), q4_word_f16(wj[j]), f4_t{0.f, 0.f, 0.f, 0.f});
-                        acc[t] += sc * p;
-                    }
-                }
-            } else if constexpr (FMT == FMT_I8) {
-#pragma unroll
-                for (int jj = 0; jj < J; ++jj) {
-                    acc[t] = mma16<FMT_F16>(x8_i8_order(u.x[2 * jj]), i8_words_f16(u.w[t][jj].x, u.w[t][jj].y), acc[t]);
-                    acc[t] = mma16<FMT_F16>(x8_i8_order(u.x[2 * jj + 1]), i8_words_f16(u.w[t][jj].z, u.w[t][jj].w), acc[t]);
-                }
-            } else {
-#pragma unroll
-                for (int jj = 0; jj < J; ++jj) acc[t] = mma16<FMT>(u.x[jj], u.w[t][jj], acc[t]);
-            }
-        }
-        if (kc + 1 == steps) {                                   /* end of a group: store, reset */
-            /* lane (c, g) holds tokens 4 g .. 4 g + 3 of row c of each tile */
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                const int64_t r = i0 + 16 * t + c;
-                float rs = 1.f;
-                if constexpr (FMT == FMT_I8) rs = f16_bits_to_f32((uint16_t)u.s[t][0]);
-                if (r < r1) {
-#pragma unroll
-                    for (int jj = 0; jj < 4; ++jj) {
-                        const int tok = 4 * g + jj;
-                        if (tok < ntok)                          /* a global (not flat) store keeps the load waits exact */
-                            as_global<g_f32*>(reinterpret_cast<char*>(d.y) + (int64_t)(token0 + tok) * d.y_stride)[r] =
-                                acc[t][jj] * rs;
-                    }
-                }
-                acc[t] = f4_t{0.f, 0.f, 0.f, 0.f};
-            }
-        }
-        if (++kc == steps) { kc = 0; ++gc; }
-    };
-    Unit buf[2];
-    load(buf[0]);
-    int64_t u = 0;                                               /* buf[0] holds unit u */
-    for (; u + 3 <= n; u += 2) {
-        load(buf[1]);                                            /* unit u + 1 */
-        __builtin_amdgcn_sched_barrier(0);
-        multiply(buf[0]);                                        /* unit u     */
-        load(buf[0]);                                            /* unit u + 2 */
-        __builtin_amdgcn_sched_barrier(0);
-        multiply(buf[1]);                                        /* unit u + 1 */
-    }
-    /* one or two units left, unit u in buf[0] */
-    if (u + 1 < n) {
-        load(buf[1]);
-        multiply(buf[0]);
-        multiply(buf[1]);
-    } else {
-        multiply(buf[0]);
-    }
-}
-
-/* The matrix-core sweep over the byte range [lo, hi) of the weight stream (groups of 16 NT rows). */
-template <int FMT, int NT>
-__device__ __forceinline__ void stream_range_mma(const DevMat* __restrict__ tab, const int64_t* __restrict__ cost,
-                                                 int nmat, int64_t lo, int64_t hi, int32_t token0, int ntok,
-                                                 int lane, int& hint) {
-    for (int m = first_matrix(cost, nmat, lo, hint); m < nmat; ++m) {
-        const DevMat d = tab[m];
-        if (d.cost0 >= hi) break;
-        hint = m;
-        const int fmt = FMT ? FMT : d.fmt;
-        const RowRange rr = range_rows(d, lo, hi, 16 * NT);
-        if (rr.r0 >= rr.r1) continue;
-        const bool short_rows = d.nc * 16 < 64 * (fmt == FMT_Q4 || fmt == FMT_I8 ? 2 : 4);   /* under one step */
-#define WSR_ROWS(F, S16, SH) rows_mma<F, NT, S16, SH>(d, rr.r0, rr.r1, token0, ntok, lane)
-        if ((FMT == 0 || FMT == FMT_F16) && fmt == FMT_F16) {
-            if (short_rows) WSR_ROWS(FMT_F16, false, true); else WSR_ROWS(FMT_F16, false, false);
-        } else if ((FMT == 0 || FMT == FMT_BF16) && fmt == FMT_BF16) {
-            if (short_rows) WSR_ROWS(FMT_BF16, false, true); else WSR_ROWS(FMT_BF16, false, false);
-        } else if ((FMT == 0 || FMT == FMT_Q4) && fmt == FMT_Q4) {
-            if (short_rows) WSR_ROWS(FMT_Q4, false, true);
-            else if (d.nc % 8 == 0 && (reinterpret_cast<uintptr_t>(d.s) & 15) == 0) WSR_ROWS(FMT_Q4, true, false);
-            else WSR_ROWS(FMT_Q4, false, false);
-        } else if ((FMT == 0 || FMT == FMT_I8) && fmt == FMT_I8) {
-            if (short_rows) WSR_ROWS(FMT_I8, false, true); else WSR_ROWS(FMT_I8, false, false);
-        }
-#undef WSR_ROWS
     }
 }
 
