@@ -13,7 +13,8 @@ Also measured in the same run and reported under "rows" (same JSON line):
   gemv_f16     4096 x 4096 fp16 GEMV, 32 distinct matrices visited per pass (1 GiB)
   llama8b_q4   decode sweep of the Llama-3-8B shape in 4-bit blocks (4.22 GB per token)
   protocol     the matched protocol's pass: int8 GEMV with fp16 row scales over 12 matrices of
-               12288 x 7168 (1.06 GB), as 12 dispatches and as one launch, plus the T-sweep
+               12288 x 7168 (1.06 GB), as 12 dispatches, as the same 12 dispatches replayed from
+               a HIP graph, and as one launch, plus the T-sweep
   endpoints    Alg. 2 over the same set stored as a file: map (pinned pages in place), resident and
                per-use copy (staged from the file pages) rates, and the endpoint it selects
   ordering     the protocol pass ordered against an in-flight framework stream by four mechanisms
@@ -386,7 +387,28 @@ def row_protocol(stream, wsr, warmup_passes=12, passes=31, tokens=16):
            "warmup_passes": warmup_passes, "timed_passes": passes,
            "paper_context_GBps": {"packed_int8_resident": 523, "pure_read_reference": 517,
                                   "note": "another machine (unified memory); context, not a target"}}
-    for name, fn in (("dispatches_12", dispatches), ("one_launch", one)):
+    # the 12 dispatches recorded once in a HIP graph and replayed per pass: the same kernels and
+    # launch shapes, without the host launching each one
+    dispatches()
+    torch.cuda.synchronize()
+    eager = [d["y"].clone() for d in sp]
+    graph = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(graph, stream=cap):
+            for d in sp:
+                wsr.wsr_gemv_i8(d["w"], d["scales"], d["x"], d["y"], d["M"], d["K"], cap)
+    torch.cuda.current_stream().wait_stream(cap)
+    replay = graph.replay
+    replays_ok = True
+    for _ in range(3):                     # each replay, with eager work between, gives the eager bits
+        for d in sp:
+            d["y"].fill_(float("nan"))
+        replay()
+        torch.cuda.synchronize()
+        replays_ok &= all(torch.equal(a, d["y"]) for a, d in zip(eager, sp))
+    for name, fn in (("dispatches_12", dispatches), ("one_launch", one), ("graph_12", replay)):
         for _ in range(warmup_passes):
             fn()
         ms = [timed(fn, 1, stream) * 1e3 for _ in range(passes)]
@@ -394,6 +416,10 @@ def row_protocol(stream, wsr, warmup_passes=12, passes=31, tokens=16):
         res[name] = {"median_ms_per_pass": st["median"], "iqr_ms": st["iqr"], "ci95_ms": st["ci95_median"],
                      "GBps_at_median": nbytes / (st["median"] * 1e-3) / 1e9,
                      "hbm_frac": nbytes / (st["median"] * 1e-3) / HBM_PEAK}
+        if name == "graph_12":
+            torch.cuda.synchronize()
+            res[name]["bitwise_equal_to_dispatches"] = bool(replays_ok) and all(
+                torch.equal(a, d["y"]) for a, d in zip(eager, sp))
         log(f"protocol {name}: median {st['median'] * 1e3:.1f} us/pass, "
             f"{res[name]['GBps_at_median']:.1f} GB/s ({res[name]['hbm_frac'] * 100:.1f}% of 8 TB/s)")
     wsr.wsr_decode_sweep(specs, tokens, ws, ws.numel(), stream)

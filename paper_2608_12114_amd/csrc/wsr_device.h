@@ -692,7 +692,7 @@ __device__ __forceinline__ void group_i8(g_u32x4* Wq, const uint16_t* S, g_u32x4
    count low enough for several waves per SIMD. */
 template <int T> struct ColsI8 { static constexpr int R = 8, U = 1; };
 /* The same for the standalone int8 GEMV kernels (one group of R rows per wave). */
-template <int T> struct GemvI8 { static constexpr int R = 4, U = 4; };
+template <int T> struct GemvI8 { static constexpr int R = 4, U = 1; };
 template <> struct GemvI8<2> { static constexpr int R = 4, U = 2; };
 template <> struct GemvI8<4> { static constexpr int R = 8, U = 1; };
 template <> struct GemvI8<8> { static constexpr int R = 8, U = 1; };

@@ -172,3 +172,39 @@ def test_mma_short_rows_unit_vectors_exact(fmt, M, K):
     for t, j in enumerate(cols):
         want = ora.gemv(dict(fmt=fmt, w=W, s=S), X[t]) if fmt in (wl.Q4, wl.I8) else ora.gemv16(W, X[t], fmt)
         assert np.array_equal(f32_bits(y[t]), f32_bits(want)), (fmt, j)
+
+
+def test_mma_edge_cases():
+    """No tokens: rejected (WSR_E_ARG) before anything is enqueued.  An empty matrix (M = 0) inside the table, an activation shared
+    by every token (x_tok_stride = 0), and 33 tokens (passes of 16, 16 and 1): every token within
+    2e-3 of the oracle, outputs past each token's M rows untouched."""
+    ora = oracle.get()
+    M, K = 40, 520
+    W, _ = host_matrix(wl.F16, M, K, seed=11)
+    Wq, Sq = host_matrix(wl.Q4, 24, 2048, seed=12)
+    T = 33
+    X = synth.normal16((T, K), wl.X_SIGMA, wl.F16, seed=11, stream=605)
+    xq = synth.normal16((1, 2048), wl.X_SIGMA, wl.F16, seed=12, stream=606)
+    w, x = dv.to_device(W), dv.to_device(X)
+    wq, sq, xqd = dv.to_device(Wq), dv.to_device(Sq), dv.to_device(xq)
+    y = torch.full((T, M + 2), float("nan"), dtype=torch.float32, device="cuda")
+    yq = torch.full((T, 24 + 2), float("nan"), dtype=torch.float32, device="cuda")
+    y0 = torch.full((T, 4), float("nan"), dtype=torch.float32, device="cuda")
+    mats = wsr.make_mats([
+        dict(fmt=wsr.WSR_F16, M=M, K=K, w=w, scales=None, x=x, x_tok_stride=K * 2, y=y, y_tok_stride=(M + 2) * 4),
+        dict(fmt=wsr.WSR_BF16, M=0, K=K, w=w, scales=None, x=x, x_tok_stride=K * 2, y=y0, y_tok_stride=16),
+        dict(fmt=wsr.WSR_Q4, M=24, K=2048, w=wq, scales=sq, x=xqd, x_tok_stride=0, y=yq, y_tok_stride=26 * 4)])
+    ws = zeros_u8(wsr.wsr_sweep_workspace_bytes(mats))
+    with pytest.raises(wsr.WsrError) as e:
+        wsr.wsr_decode_sweep_mma(mats, 0, ws, ws.numel(), stream())
+    assert e.value.status == wsr.WSR_E_ARG
+    torch.cuda.synchronize()
+    assert torch.isnan(y).all() and torch.isnan(yq).all()
+    wsr.wsr_decode_sweep_mma(mats, T, ws, ws.numel(), stream())
+    torch.cuda.synchronize()
+    a, b = y.cpu().numpy(), yq.cpu().numpy()
+    assert np.isnan(a[:, M:]).all() and np.isnan(b[:, 24:]).all() and torch.isnan(y0).all()
+    want_q = ora.gemv(dict(fmt=wl.Q4, w=Wq, s=Sq), xq[0])
+    for t in range(T):
+        assert rel_l2(a[t, :M], ora.gemv16(W, X[t], wl.F16)) <= TOL, t
+        assert rel_l2(b[t, :24], want_q) <= TOL, t
