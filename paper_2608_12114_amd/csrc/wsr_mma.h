@@ -127,6 +127,25 @@ constexpr int mma_x_byte(int s) { return FMT == FMT_I8 ? 128 * (s / 2) + 16 * (s
 
 __device__ __forceinline__ u32x4 keep_if(bool ok, u32x4 v) { return ok ? v : zero4(); }
 
+/* Raw buffer access: a wave-uniform base in a scalar resource, a 32-bit lane offset, a scalar
+   offset and an immediate, with no per-lane address arithmetic.  Every access here is in bounds
+   by construction, so the resource's range check is left open (num_records = 2^32 - 1); the word
+   0x00020000 is the gfx9 family's format for untyped buffer access.  aux 2 marks a load
+   non-temporal (read once). */
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+__device__ __forceinline__ rsrc_t buffer_of(const void* base) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, -1, 0x00020000);
+}
+__device__ __forceinline__ u32x4 buf_once(rsrc_t r, uint32_t v, uint32_t s) {
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, v, s, 2));
+}
+__device__ __forceinline__ u32x4 buf_reused(rsrc_t r, uint32_t v, uint32_t s) {
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, v, s, 0));
+}
+__device__ __forceinline__ uint32_t buf_u16(rsrc_t r, uint32_t v, uint32_t s) {
+    return __builtin_amdgcn_raw_buffer_load_b16(r, v, s, 0);
+}
+
 /* A wave-uniform pointer held in scalar registers, so that a load from it plus a 32-bit lane
    offset and a constant takes the scalar-base form (no per-lane address arithmetic). */
 __device__ __forceinline__ const char* uniform_ptr(const char* p) {
@@ -161,7 +180,7 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
     const int64_t ngroups = (r1 - r0 + 16 * NT - 1) / (16 * NT);
     const int64_t n = ngroups * steps;                           /* units */
     if (n == 0) return;
-    const char* xb = static_cast<const char*>(d.x) + (int64_t)token0 * d.x_stride;   /* uniform */
+    const rsrc_t rx = buffer_of(uniform_ptr(static_cast<const char*>(d.x) + (int64_t)token0 * d.x_stride));
     const uint32_t vx = (uint32_t)((c < ntok ? c : 0) * d.x_stride) + XG * g;
     const int64_t srow = FMT == FMT_Q4 ? nc * 2 : 2;             /* scale bytes per row */
     f4_t acc[NT];
@@ -169,14 +188,14 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
     for (int t = 0; t < NT; ++t) acc[t] = f4_t{0.f, 0.f, 0.f, 0.f};
     int64_t gl = 0, gc = 0;                                      /* group of the next unit to load, multiply */
     int32_t kl = 0, kc = 0;                                      /* and its step                             */
-    const char* wg = nullptr;                                    /* this group's row r0 of codes, scales */
-    const char* sg = nullptr;
+    rsrc_t rw = buffer_of(d.w), rs = buffer_of(d.w);             /* this group's row r0 of codes, scales */
     uint32_t vr[NT], vs[NT];                                     /* lane offsets: row of each tile */
     auto load = [&](Unit& u) {
         if (kl == 0) {
             const int64_t i0 = r0 + gl * 16 * NT;
-            wg = static_cast<const char*>(d.w) + i0 * crb;
-            sg = static_cast<const char*>(d.s) + i0 * srow;
+            rw = buffer_of(uniform_ptr(static_cast<const char*>(d.w) + i0 * crb));
+            if constexpr (FMT == FMT_Q4 || FMT == FMT_I8)
+                rs = buffer_of(uniform_ptr(static_cast<const char*>(d.s) + i0 * srow));
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
                 const int64_t rr = std::min<int64_t>(i0 + 16 * t + c, r1 - 1) - i0;
@@ -185,47 +204,43 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
             }
         }
         if constexpr (!SHORT) {
-            const int64_t kb = std::min<int64_t>((int64_t)kl * SB, crb - SB);   /* the last step ends at the row's end */
-            const char* ws = uniform_ptr(wg + kb);
-            const char* xs = uniform_ptr(xb + std::min<int64_t>((int64_t)kl * SK, kelem - SK) * 2);
+            /* the last step ends at the row's end; offsets stay below 2^31 (the caller's limits) */
+            const uint32_t kb = (uint32_t)std::min<int64_t>((int64_t)kl * SB, crb - SB);
+            const uint32_t xo = (uint32_t)(std::min<int64_t>((int64_t)kl * SK, kelem - SK) * 2);
 #pragma unroll
             for (int t = 0; t < NT; ++t)
 #pragma unroll
-                for (int jj = 0; jj < J; ++jj)
-                    u.w[t][jj] = load_once(as_global<g_u32x4*>(ws + (vr[t] + 16 * g) + 64 * jj));
+                for (int jj = 0; jj < J; ++jj) u.w[t][jj] = buf_once(rw, vr[t] + 16 * g + 64 * jj, kb);
 #pragma unroll
-            for (int s = 0; s < SL; ++s) u.x[s] = load_reused(as_global<g_u32x4*>(xs + vx + mma_x_byte<FMT>(s)));
+            for (int s = 0; s < SL; ++s) u.x[s] = buf_reused(rx, vx + mma_x_byte<FMT>(s), xo);
         } else {                                                 /* one step, shorter than SB: clamp per lane */
 #pragma unroll
             for (int t = 0; t < NT; ++t)
 #pragma unroll
-                for (int jj = 0; jj < J; ++jj) {
-                    const uint32_t o = (uint32_t)std::min<int64_t>(64 * jj + 16 * g, crb - 16);
-                    u.w[t][jj] = load_once(as_global<g_u32x4*>(uniform_ptr(wg) + (vr[t] + o)));
-                }
+                for (int jj = 0; jj < J; ++jj)
+                    u.w[t][jj] = buf_once(rw, vr[t] + (uint32_t)std::min<int64_t>(64 * jj + 16 * g, crb - 16), 0);
 #pragma unroll
             for (int s = 0; s < SL; ++s) {
                 const int64_t e = std::min<int64_t>((XG * g + mma_x_byte<FMT>(s)) / 2, kelem - 8);
-                u.x[s] = load_reused(as_global<g_u32x4*>(uniform_ptr(xb) + (vx - XG * g + (uint32_t)(2 * e))));
+                u.x[s] = buf_reused(rx, vx - XG * g + (uint32_t)(2 * e), 0);
             }
         }
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             if constexpr (FMT == FMT_Q4) {
-                const int64_t b0 = SHORT ? 0 : std::min<int64_t>((int64_t)kl * 8, nc - 8);   /* the step's first block */
+                const uint32_t b0 = SHORT ? 0 : (uint32_t)std::min<int64_t>((int64_t)kl * 8, nc - 8);   /* first block */
                 if constexpr (SCALE16) {
-                    const u32x4 v = load_reused(as_global<g_u32x4*>(uniform_ptr(sg + b0 * 2) + vs[t]));
+                    const u32x4 v = buf_reused(rs, vs[t], b0 * 2);
                     u.s[t][0] = v.x, u.s[t][1] = v.y, u.s[t][2] = v.z, u.s[t][3] = v.w;
                 } else {
                     uint32_t h[8];
 #pragma unroll
-                    for (int j = 0; j < 8; ++j)
-                        h[j] = *as_global<g_u16*>(uniform_ptr(sg + std::min<int64_t>(b0 + j, nc - 1) * 2) + vs[t]);
+                    for (int j = 0; j < 8; ++j) h[j] = buf_u16(rs, vs[t], (uint32_t)std::min<int64_t>(b0 + j, nc - 1) * 2);
 #pragma unroll
                     for (int j = 0; j < 4; ++j) u.s[t][j] = h[2 * j] | h[2 * j + 1] << 16;
                 }
             } else if constexpr (FMT == FMT_I8) {
-                u.s[t][0] = *as_global<g_u16*>(uniform_ptr(sg) + vs[t]);
+                u.s[t][0] = buf_u16(rs, vs[t], 0);
             }
         }
         if (++kl == steps) { kl = 0; ++gl; }
@@ -234,7 +249,8 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
         const int64_t i0 = r0 + gc * 16 * NT;
         /* the step's first weight, and the first one it has not already covered */
         const int64_t e0 = SHORT ? 0 : std::min<int64_t>((int64_t)kc * SK, kelem - SK), e1 = SHORT ? 0 : (int64_t)kc * SK;
-        if (SHORT || e0 < e1) {                                  /* a moved-back or short last step */
+        if (__builtin_expect(SHORT || e0 < e1, 0)) {             /* a moved-back or short last step */
+            __asm__ volatile("" ::: "memory");                   /* kept a branch, not selects run every step */
 #pragma unroll
             for (int s = 0; s < SL; ++s) {
                 const int64_t e = e0 + (XG * g + mma_x_byte<FMT>(s)) / 2;
