@@ -399,7 +399,7 @@ def row_protocol(stream, wsr, warmup_passes=12, passes=31, tokens=16):
     # launch shapes, without the host launching each one
     dispatches()
     torch.cuda.synchronize()
-    eager = [d["y"].clone() for d in sp]
+    eager = [d["y"][0].clone() for d in sp]   # a single-token GEMV writes token 0's outputs only
     graph = torch.cuda.CUDAGraph()
     cap = torch.cuda.Stream()
     cap.wait_stream(torch.cuda.current_stream())
@@ -412,10 +412,10 @@ def row_protocol(stream, wsr, warmup_passes=12, passes=31, tokens=16):
     replays_ok = True
     for _ in range(3):                     # each replay, with eager work between, gives the eager bits
         for d in sp:
-            d["y"].fill_(float("nan"))
+            d["y"][0].fill_(float("nan"))
         replay()
         torch.cuda.synchronize()
-        replays_ok &= all(torch.equal(a, d["y"]) for a, d in zip(eager, sp))
+        replays_ok &= all(torch.equal(a, d["y"][0]) for a, d in zip(eager, sp))
     for name, fn in (("dispatches_12", dispatches), ("one_launch", one), ("graph_12", replay)):
         for _ in range(warmup_passes):
             fn()
@@ -427,7 +427,7 @@ def row_protocol(stream, wsr, warmup_passes=12, passes=31, tokens=16):
         if name == "graph_12":
             torch.cuda.synchronize()
             res[name]["bitwise_equal_to_dispatches"] = bool(replays_ok) and all(
-                torch.equal(a, d["y"]) for a, d in zip(eager, sp))
+                torch.equal(a, d["y"][0]) for a, d in zip(eager, sp))
         log(f"protocol {name}: median {st['median'] * 1e3:.1f} us/pass, "
             f"{res[name]['GBps_at_median']:.1f} GB/s ({res[name]['hbm_frac'] * 100:.1f}% of 8 TB/s)")
     wsr.wsr_decode_sweep(specs, tokens, ws, ws.numel(), stream)
