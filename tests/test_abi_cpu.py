@@ -198,6 +198,12 @@ def test_sweep_mma_argument_checks():
     assert _status(f, mats, 0, 4, None, 0, None) == wsr.WSR_OK                   # empty sweep
     shared = wsr.make_mats([dict(good, y_tok_stride=16)])
     assert _status(f, shared, 1, 2, A, ws, None) == wsr.WSR_E_ARG                # tokens would share y
+    # 64 rows and 16 tokens must stay within 32-bit lane offsets
+    long_row = wsr.make_mats([dict(good, fmt=2, scales=None, M=1, K=(1 << 24) + 8, x_tok_stride=(1 << 25) + 16)])
+    assert _status(f, long_row, 1, 1, A, ws, None) == wsr.WSR_E_SIZE             # row above 32 MiB
+    assert "32 MiB" in wsr.wsr_last_error()
+    wide_x = wsr.make_mats([dict(good, x_tok_stride=(1 << 27) + 16)])
+    assert _status(f, wide_x, 1, 1, A, ws, None) == wsr.WSR_E_SIZE               # token stride above 128 MiB
 
 
 def test_register_argument_checks():

@@ -78,9 +78,9 @@ def test_mma_matrix_parity_and_bounds(fmt, T):
         assert rel_l2(y[t, :M], want) <= TOL, (fmt, t)
 
 
-def sweep_pair(inp, tokens):
+def sweep_pair(inp, tokens, chained=False):
     """(vector-ALU sweep outputs, matrix-core sweep outputs) for the same inputs."""
-    mats = wsr.make_mats(inp.specs())
+    mats = wsr.make_mats(inp.specs(chained=chained))
     ws = zeros_u8(wsr.wsr_sweep_workspace_bytes(mats))
     for y in inp.y:
         y.fill_(float("nan"))
@@ -94,11 +94,14 @@ def sweep_pair(inp, tokens):
     return valu, [y.clone() for y in inp.y]
 
 
-def test_mma_mixed_sweep():
+@pytest.mark.parametrize("chained", [False, True], ids=["one_launch", "chained"])
+def test_mma_mixed_sweep(chained):
+    """Chained: each layer's activation slots depend on earlier outputs, so every pass is several
+    launches (one per run of independent matrices)."""
     mats = wl.decode_matrices(dv.small_model(layers=4, d=512, ffn=1536, vocab=3000))
     fmts = [(wl.I8, wl.Q4, wl.BF16, wl.F16, wl.Q4)[m.layer] for m in mats]
     inp = dv.SweepInputs(mats, fmts, tokens=19)
-    valu, mma = sweep_pair(inp, 19)
+    valu, mma = sweep_pair(inp, 19, chained)
     ora = oracle.get()
     for i, (m, fmt) in enumerate(zip(mats, fmts)):
         a, b = valu[i].cpu().numpy(), mma[i].cpu().numpy()
