@@ -444,15 +444,17 @@ struct StageEvents {
 };
 StageEvents g_stage_ev[64];
 
-hipError_t stage_events(int dev, StageEvents*& out) {
-    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-    StageEvents& e = g_stage_ev[dev];
-    out = &e;
+/* Creates the events on first use; the caller holds e.mu.  A failed creation destroys the events it
+   made, so a later call starts again from nothing. */
+hipError_t make_stage_events(StageEvents& e) {
     if (e.made) return hipSuccess;
     hipEvent_t* all[5] = {&e.start, &e.copied[0], &e.copied[1], &e.consumed[0], &e.consumed[1]};
-    for (hipEvent_t* p : all) {
-        const hipError_t r = hipEventCreateWithFlags(p, hipEventDisableTiming);
-        if (r != hipSuccess) return r;
+    for (int i = 0; i < 5; ++i) {
+        const hipError_t r = hipEventCreateWithFlags(all[i], hipEventDisableTiming);
+        if (r != hipSuccess) {
+            for (int j = 0; j < i; ++j) (void)hipEventDestroy(*all[j]);
+            return r;
+        }
     }
     e.made = true;
     return hipSuccess;
@@ -502,10 +504,10 @@ wsr_status wsr_sweep_staged(const wsr_mat* mats, int32_t n, int32_t token, void*
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "sweep_staged: device");
-    StageEvents* ev = nullptr;
-    e = stage_events(dev, ev);
-    if (e != hipSuccess) return hip_fail(e, "sweep_staged: events");
-    std::lock_guard<std::mutex> lock(ev->mu);
+    if (dev < 0 || dev >= 64) return fail(WSR_E_ARG, "sweep_staged: device %d", dev);
+    StageEvents* ev = &g_stage_ev[dev];
+    std::lock_guard<std::mutex> lock(ev->mu);       /* held from the events' creation on */
+    if ((e = make_stage_events(*ev)) != hipSuccess) return hip_fail(e, "sweep_staged: events");
     hipStream_t s = static_cast<hipStream_t>(stream), cs = static_cast<hipStream_t>(copy_stream);
     char* buf[2] = {static_cast<char*>(stage), static_cast<char*>(stage) + half};
     /* The first copy waits for the work already on `stream` (an earlier reader of the buffer). */
@@ -668,9 +670,12 @@ wsr_status wsr_decode_sweep_ordered(const wsr_mat* mats, int32_t n, int32_t n_to
     OrderEvents& ev = g_order_ev[dev];
     std::lock_guard<std::mutex> lock(ev.mu);
     if (!ev.made) {
-        if ((e = hipEventCreateWithFlags(&ev.before, hipEventDisableTiming)) != hipSuccess ||
-            (e = hipEventCreateWithFlags(&ev.after, hipEventDisableTiming)) != hipSuccess)
+        if ((e = hipEventCreateWithFlags(&ev.before, hipEventDisableTiming)) != hipSuccess)
             return hip_fail(e, "decode_sweep_ordered: events");
+        if ((e = hipEventCreateWithFlags(&ev.after, hipEventDisableTiming)) != hipSuccess) {
+            (void)hipEventDestroy(ev.before);
+            return hip_fail(e, "decode_sweep_ordered: events");
+        }
         ev.made = true;
     }
     hipStream_t fs = static_cast<hipStream_t>(framework_stream), os = static_cast<hipStream_t>(own_stream);

@@ -128,3 +128,38 @@ def test_staged_protocol_size():
     got = run_staged(inp, specs, 1, 64 << 20)
     for a, b in zip(want, got):
         assert np.array_equal(f32_bits(a), f32_bits(b))
+
+
+def test_staged_from_several_threads(model):
+    """Four host threads run staged sweeps at once, each with its own streams, staging buffer and
+    outputs, from the same pinned sources: the per-device events are created once and every call's
+    enqueueing is serialised, so each thread gets the resident outputs bit for bit."""
+    import threading
+    want = resident(model, 3)
+    src = host_sources(model, True)
+    base = staged_specs(model, src)
+    outs, errs = [], []
+    jobs = []
+    for _ in range(4):
+        ys = [torch.full_like(y, float("nan")) for y in model.y]
+        specs = [dict(s, y=y) for s, y in zip(base, ys)]
+        jobs.append((wsr.make_mats(specs), ys, zeros_u8(96 << 10), torch.cuda.Stream(), torch.cuda.Stream()))
+    torch.cuda.synchronize()
+
+    def work(mats, stage, s, cs):
+        try:
+            for t in range(3):
+                wsr.wsr_sweep_staged(mats, t, stage, stage.numel(), s, cs)
+        except Exception as e:          # reported below, on the test's thread
+            errs.append(e)
+
+    threads = [threading.Thread(target=work, args=(m, st, s, cs)) for m, _, st, s, cs in jobs]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    torch.cuda.synchronize()
+    assert not errs, errs
+    for k, (_, ys, *_rest) in enumerate(jobs):
+        for i, (a, y) in enumerate(zip(want, ys)):
+            assert np.array_equal(f32_bits(a), f32_bits(y.cpu().numpy())), (k, i)
