@@ -12,6 +12,7 @@
 #include "wsr_device.h"
 
 namespace wsr {
+
 /* Rows [r0, r1) of matrix d that the byte range [lo, hi) of the weight stream covers.  A byte
    boundary maps to the first group of g rows starting at or after it, the same way for the ranges
    on both sides, so the ranges still cover each row once and break only between whole groups. */
@@ -30,8 +31,8 @@ __device__ __forceinline__ RowRange range_rows(const DevMat& d, int64_t lo, int6
    weight pair per token, and from about four tokens on the vector ALUs, not HBM, set the rate.
    These loops hand the products to the matrix cores instead.  A wave owns tiles of 16 rows; per
    32-element slab of K it forms D = X^T W^T for the tile with one v_mfma_f32_16x16x32: the A
-   operand holds 16 token columns of activations (columns past the pass's tokens are zero), the B
-   operand 16 weight rows decoded to fp16.  Decoded weights are exact: q4 and int8 codes become the
+   operand holds 16 token slots of activations (slots past the pass's tokens repeat its first token
+   and their results are never stored), the B operand 16 weight rows decoded to fp16.  Decoded weights are exact: q4 and int8 codes become the
    small integers q as 1024 + (q + bias) formed by one bit operation, minus 1024 + bias by one packed
    fp16 subtraction; 16-bit weights are used as stored.  Every product q x is exact in fp32, and
    the scales multiply the fp32 slab sums, but the matrix core adds a slab's products in an order of
@@ -40,8 +41,8 @@ __device__ __forceinline__ RowRange range_rows(const DevMat& d, int64_t lo, int6
    D[4(i/16)+j][i%16].  K may be permuted inside a slab as long as A and B follow the same order;
    the decoders give (k0,k4,k1,k5,k2,k6,k3,k7) for a q4 word and (k0,k2,k1,k3,k4,k6,k5,k7) for two
    int8 words, and the activation loaders permute x to match.  A q4 scale covers one block of 32, so
-   a slab is one block: the four words a lane loaded (block b0 + i/16 of row i%16) are transposed
-   between the four 16-lane groups with two rounds of lane swaps, and each block's product is formed
+   a slab is one block: the four words a lane loaded in chunk jj (block b0 + 4 jj + i/16 of row i%16) are
+   transposed between the four 16-lane groups with two rounds of lane swaps, and each block's product is formed
    alone and added with its row's scale.  int8 scales are per row and multiply the finished sum. */
 typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 b8_t __attribute__((ext_vector_type(8)));
