@@ -16,6 +16,7 @@
 
 #include "wsr.h"
 #include "wsr_internal.h"
+#include "wsr_mma_launch.h"
 
 using wsr::DevMat;
 
@@ -625,15 +626,18 @@ extern "C" wsr_status wsr_decode_sweep_mma(const wsr_mat* mats, int32_t n, int32
                                                 ((size_t)n * sizeof(DevMat) + 255) / 256 * 256);
     hipError_t e = wsr::launch_put_table(dtab, dcost, p.tab.data(), n, ctr, s);
     if (e != hipSuccess) return hip_fail(e, "decode_sweep_mma: table upload");
-    std::vector<int64_t> max_group(p.segs.size(), 0);
+    std::vector<int64_t> max_group(p.segs.size(), 0), max_tail(p.segs.size(), 0);
     for (size_t i = 0; i < p.segs.size(); ++i)
-        for (int m = p.segs[i].first; m < p.segs[i].first + p.segs[i].count; ++m)
+        for (int m = p.segs[i].first; m < p.segs[i].first + p.segs[i].count; ++m) {
             max_group[i] = std::max(max_group[i], p.tab[m].row_bytes * std::min(p.tab[m].M, wsr::mma_group_rows()));
+            max_tail[i] = std::max(max_tail[i], p.tab[m].row_bytes * std::min(p.tab[m].M, wsr::mma_tail_rows()));
+        }
     for (int32_t t = 0; t < n_tokens; t += 16) {
         const int ntok = std::min<int32_t>(16, n_tokens - t);
         for (size_t i = 0; i < p.segs.size(); ++i) {
             const Seg& g = p.segs[i];
-            e = wsr::launch_sweep_mma(dtab + g.first, dcost + g.first, g.count, g.total, max_group[i], g.fmt, t, ntok, s);
+            e = wsr::launch_sweep_mma(dtab + g.first, dcost + g.first, g.count, g.total, max_group[i], max_tail[i], g.fmt,
+                                      t, ntok, s);
             if (e != hipSuccess) return hip_fail(e, "decode_sweep_mma: launch");
         }
     }

@@ -40,11 +40,6 @@ hipError_t launch_gemv(const DevMat& m, hipStream_t s);
    m.x_stride and m.y_stride are the column strides in bytes. */
 hipError_t launch_gemv_cols(const DevMat& m, int T, hipStream_t s);
 /* Writes the table and clears the two tile counters at ctr (ctr may be null). */
-/* Tokens token0 .. token0 + ntok - 1 (ntok <= 16) of the sweep on the matrix cores; max_group is
-   the largest row group's weight-stream bytes (mma_group_rows() rows of any matrix in the table). */
-int64_t mma_group_rows();
-hipError_t launch_sweep_mma(const DevMat* tab, const int64_t* cost, int nmat, int64_t total, int64_t max_group,
-                            int fmt_all, int32_t token0, int ntok, hipStream_t s);
 hipError_t launch_put_table(DevMat* dst, int64_t* cost, const DevMat* src, int n, unsigned* ctr,
                             hipStream_t s);
 /* One pass over the table's weights for tokens token .. token + T - 1 (T = 1, 2, 4, 8, 16; at most

@@ -342,14 +342,20 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
 /* The matrix-core sweep over the byte range [lo, hi) of the weight stream (groups of 16 NT rows). */
 template <int FMT, int NT>
 __device__ __forceinline__ void stream_range_mma(const DevMat* __restrict__ tab, const int64_t* __restrict__ cost,
-                                                 int nmat, int64_t lo, int64_t hi, int32_t token0, int ntok,
-                                                 int lane, int& hint) {
+                                                 int nmat, int64_t lo, int64_t hi, int64_t tail, int64_t main_rows,
+                                                 int32_t token0, int ntok, int lane, int& hint) {
     for (int m = first_matrix(cost, nmat, lo, hint); m < nmat; ++m) {
         const DevMat d = tab[m];
         if (d.cost0 >= hi) break;
         hint = m;
         const int fmt = FMT ? FMT : d.fmt;
-        const RowRange rr = range_rows(d, lo, hi, 16 * NT);
+        RowRange rr = range_rows(d, lo, hi, 16 * NT);
+        if (tail > 0) {              /* rows below the main region's last boundary are not the tail's */
+            const int64_t fl = tail > d.cost0 ? ceil_div(tail - d.cost0, d.row_bytes * main_rows) * main_rows : 0;
+            const int64_t f = fl < d.M ? fl : d.M;
+            rr.r0 = rr.r0 > f ? rr.r0 : f;
+            rr.r1 = rr.r1 > f ? rr.r1 : f;
+        }
         if (rr.r0 >= rr.r1) continue;
         const bool short_rows = d.nc * 16 < 64 * (fmt == FMT_Q4 || fmt == FMT_I8 ? 2 : 4);   /* under one step */
 #define WSR_ROWS(F, S16, SH) rows_mma<F, NT, S16, SH>(d, rr.r0, rr.r1, token0, ntok, lane)

@@ -7,40 +7,101 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "wsr_mma.h"
+#include "wsr_mma_launch.h"
 
 namespace wsr {
 
 constexpr int MMA_TILES = 4;                  /* 16-row tiles per wave and row group (64 rows)     */
+constexpr int MMA_TAIL_TILES = 1;             /* ... in the tail of the stream (16 rows)           */
 constexpr int64_t SWEEP_SPAN_MMA = 64 << 10;  /* least bytes of the weight stream per wave         */
 
-/* One wave per workgroup, so that a wave whose span holds no row group frees its slot at once. */
+/* One wave per workgroup, so that a wave whose span holds no row group frees its slot at once.
+   Waves w < w1 split the stream's bytes [0, tail) into equal spans of whole 64-row groups; the
+   others split [tail, total) into spans of 16-row groups.  The launcher sets a tail only where the
+   64-row spans would leave the last round of wave slots at most a quarter full (the protocol pass:
+   2,304 groups on 2,048 slots); then the last waves to finish hold a quarter of a group's work.
+   A matrix's rows from the first 64-row boundary at or after byte `tail` on belong to the tail,
+   the rows before it to the main spans. */
 template <int FMT>
 __global__ __launch_bounds__(WAVE) void k_sweep_mma(const DevMat* __restrict__ tab, const int64_t* __restrict__ cost,
-                                                    int nmat, int64_t total, int32_t token0, int ntok) {
+                                                    int nmat, int64_t total, int64_t tail, int64_t w1,
+                                                    int32_t token0, int ntok) {
     const int lane = threadIdx.x;
-    const int64_t nw = gridDim.x, w = blockIdx.x;
-    const int64_t q = total / nw, r = total % nw;
-    const int64_t lo = q * w + (int64_t)((uint64_t)r * (uint64_t)w / nw);
-    const int64_t hi = q * (w + 1) + (int64_t)((uint64_t)r * (uint64_t)(w + 1) / nw);
+    const int64_t w = blockIdx.x;
+    const bool main = w < w1;
+    const int64_t base = main ? 0 : tail, len = main ? tail : total - tail;
+    const int64_t nw = main ? w1 : (int64_t)gridDim.x - w1, k = main ? w : w - w1;
+    const int64_t q = len / nw, r = len % nw;
+    const int64_t lo = base + q * k + (int64_t)((uint64_t)r * (uint64_t)k / nw);
+    const int64_t hi = base + q * (k + 1) + (int64_t)((uint64_t)r * (uint64_t)(k + 1) / nw);
     int hint = 0;
-    if (lo < hi) stream_range_mma<FMT, MMA_TILES>(tab, cost, nmat, lo, hi, token0, ntok, lane, hint);
+    if (lo >= hi) return;
+    if (main)
+        stream_range_mma<FMT, MMA_TILES>(tab, cost, nmat, lo, hi, 0, 16 * MMA_TILES, token0, ntok, lane, hint);
+    else
+        stream_range_mma<FMT, MMA_TAIL_TILES>(tab, cost, nmat, lo, hi, tail, 16 * MMA_TILES, token0, ntok, lane, hint);
 }
 
 int64_t mma_group_rows() { return 16 * MMA_TILES; }
+int64_t mma_tail_rows() { return 16 * MMA_TAIL_TILES; }
+
+/* Wave slots of the device for the kernel of format fmt_all (its occupancy times the CU count),
+   found once per device and format. */
+static hipError_t mma_slots(int fmt_all, int64_t& slots) {
+    static std::mutex mu;
+    static int64_t cache[64][5] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const int f = fmt_all >= 0 && fmt_all <= 4 ? fmt_all : 0;
+    std::lock_guard<std::mutex> lock(mu);
+    if (dev >= 0 && dev < 64 && cache[dev][f] > 0) {
+        slots = cache[dev][f];
+        return hipSuccess;
+    }
+    int cus = 0, per_cu = 0;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+    switch (f) {
+        case FMT_F16: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_sweep_mma<FMT_F16>, WAVE, 0); break;
+        case FMT_BF16: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_sweep_mma<FMT_BF16>, WAVE, 0); break;
+        case FMT_Q4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_sweep_mma<FMT_Q4>, WAVE, 0); break;
+        case FMT_I8: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_sweep_mma<FMT_I8>, WAVE, 0); break;
+        default: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_sweep_mma<0>, WAVE, 0); break;
+    }
+    if (e != hipSuccess) return e;
+    slots = (int64_t)cus * per_cu;
+    if (dev >= 0 && dev < 64) cache[dev][f] = slots;
+    return hipSuccess;
+}
 
 hipError_t launch_sweep_mma(const DevMat* tab, const int64_t* cost, int nmat, int64_t total, int64_t max_group,
-                            int fmt_all, int32_t token0, int ntok, hipStream_t s) {
+                            int64_t max_tail_group, int fmt_all, int32_t token0, int ntok, hipStream_t s) {
     if (nmat == 0 || total == 0) return hipSuccess;
     if (ntok < 1 || ntok > MMA_TOKENS) return hipErrorInvalidValue;
     /* a wave's span holds at least the largest row group: a row group is never split, so a smaller
        span leaves most waves without one */
     const int64_t span = std::max(SWEEP_SPAN_MMA, max_group);
+    const int64_t span_t = std::max(SWEEP_SPAN_MMA / 4, max_tail_group);
     const int64_t waves = (total + span - 1) / span;
-    if (waves > INT32_MAX) return hipErrorInvalidValue;
-#define WSR_MMA(F) \
-    hipLaunchKernelGGL((k_sweep_mma<F>), dim3((unsigned)waves), dim3(WAVE), 0, s, tab, cost, nmat, total, token0, ntok)
+    int64_t slots = 0;
+    const hipError_t e = mma_slots(fmt_all, slots);
+    if (e != hipSuccess) return e;
+    /* whole rounds of spans, and a tail only where the last round would be at most a quarter full
+       (measured on int8 passes: 1/8 full 323 -> 265 us per pass with the tail; 1/2 full 356 -> 381) */
+    int64_t tail = total, w1 = waves, w2 = 0;
+    const int64_t rounds = slots > 0 ? waves / slots : 0, rest = slots > 0 ? waves % slots : 0;
+    if (rounds >= 1 && rounds < 8 && rest > 0 && 4 * rest <= slots) {
+        tail = rounds * slots * span;
+        w1 = rounds * slots;
+        w2 = (total - tail + span_t - 1) / span_t;
+    }
+    if (w1 + w2 > INT32_MAX) return hipErrorInvalidValue;
+#define WSR_MMA(F)                                                                                              \
+    hipLaunchKernelGGL((k_sweep_mma<F>), dim3((unsigned)(w1 + w2)), dim3(WAVE), 0, s, tab, cost, nmat, total, tail, \
+                       w1, token0, ntok)
     switch (fmt_all) {
         case FMT_F16: WSR_MMA(FMT_F16); break;
         case FMT_BF16: WSR_MMA(FMT_BF16); break;

@@ -1,0 +1,21 @@
+/*
+ * wsr_mma_launch.h - launcher of the batched decode sweep on the matrix cores (defined in wsr_mma.hip).
+ */
+#ifndef WSR_MMA_LAUNCH_H
+#define WSR_MMA_LAUNCH_H
+
+#include "wsr_internal.h"
+
+namespace wsr {
+
+/* Tokens token0 .. token0 + ntok - 1 (ntok <= 16) of the sweep on the matrix cores; max_group and
+   max_tail_group are the largest row group's weight-stream bytes (mma_group_rows() rows, and
+   mma_tail_rows() rows for the tail of the stream, of any matrix in the table). */
+int64_t mma_group_rows();
+int64_t mma_tail_rows();
+hipError_t launch_sweep_mma(const DevMat* tab, const int64_t* cost, int nmat, int64_t total, int64_t max_group,
+                            int64_t max_tail_group, int fmt_all, int32_t token0, int ntok, hipStream_t s);
+
+}  // namespace wsr
+
+#endif
