@@ -211,3 +211,28 @@ def test_mma_edge_cases():
     for t in range(T):
         assert rel_l2(a[t, :M], ora.gemv16(W, X[t], wl.F16)) <= TOL, t
         assert rel_l2(b[t, :24], want_q) <= TOL, t
+
+
+def test_mma_mixed_full_size_tail():
+    """Four int8 and four bf16 matrices of 12288 x 7168 (1.06 GB), interleaved, 16 tokens: about 1,150
+    spans of the largest 64-row group, just past one round of the mixed-format kernel's wave slots,
+    so the stream ends in a tail of 16-row groups.  Every matrix against the vector-ALU sweep, and
+    sampled rows against the oracle for the first and last token."""
+    mats = wl.protocol_matrices(n=8)
+    fmts = [wl.I8 if i % 2 == 0 else wl.BF16 for i in range(8)]
+    inp = dv.SweepInputs(mats, fmts, tokens=16)
+    valu, mma = sweep_pair(inp, 16)
+    ora = oracle.get()
+    for i, (m, fmt) in enumerate(zip(mats, fmts)):
+        assert rel_l2(mma[i].cpu().numpy(), valu[i].cpu().numpy()) <= 5e-5, (m.name, fmt)
+        rows = np.unique(np.linspace(0, m.M - 1, 4).astype(np.int64))
+        for t in (0, 15):
+            x = inp.host_x(i, t)
+            got = mma[i][t].cpu().numpy()[rows]
+            want = []
+            for r in rows:
+                hw = inp.host_weights(i, int(r), 1)
+                want.append((ora.gemv(dict(fmt=fmt, w=hw[0], s=hw[1]), x) if fmt == wl.I8 else ora.gemv16(hw, x, fmt))[0])
+            assert rel_l2(got, np.array(want)) <= TOL, (m.name, fmt, t)
+    del inp, valu, mma
+    torch.cuda.empty_cache()
