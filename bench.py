@@ -290,7 +290,18 @@ def cpu_baseline(inp, bpt, seconds):
             break
     rate = nbytes / spent
     log(f"cpu oracle: {nbytes / 1e9:.2f} GB in {spent:.1f} s on {threads} threads -> {rate / 1e9:.2f} GB/s")
+    # the second mode: one thread, on the first matrix
+    hw = inp.host_weights(0)
+    x = inp.host_x(0, 0)
+    t0 = time.perf_counter()
+    oracle_gemv(ora, inp.fmts[0], hw, x, 1)
+    one = time.perf_counter() - t0
+    m0 = inp.mats[0]
+    rate1 = wl.matrix_bytes(m0.M, m0.K, inp.fmts[0]) / one
+    log(f"cpu oracle, one thread: L{m0.layer}.{m0.name} in {one:.2f} s -> {rate1 / 1e9:.2f} GB/s")
     return {"value": rate / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "single_thread": {"value": rate1 / 1e9, "unit": "GB/s", "cores": 1, "seconds": one,
+                              "sample": f"token 0, L{m0.layer}.{m0.name} ({m0.M} x {m0.K})"},
             "tokens_per_s": rate / bpt, "seconds": spent,
             "sample": f"token 0, first {len(names)} matrices in sweep order ({names[0]} .. {names[-1]}), "
                       f"{nbytes / 1e9:.2f} GB of weights, fp64 oracle with OpenMP over rows"}
