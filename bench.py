@@ -683,6 +683,35 @@ def row_size_sweep(stream, wsr):
             torch.cuda.empty_cache()
     finally:
         wsr.wsr_unregister_host(host)
+    return {"points": out, "crossovers": size_crossovers(out)}
+
+
+def size_crossovers(pts):
+    """The size sweep's three crossovers (Sec. 3.4's matrix-size sweep): (i) dispatch, the smallest
+    size whose resident rate reaches half the plateau; (ii) MALL, the smallest size from which the
+    single-buffer repeat rate stays within 2 % of the rotated rate (below it the repeated buffer
+    is served partly from the 256 MB Infinity Cache); (iii) the first size where a host-mapped pass
+    is as fast as a resident one (none expected across PCIe)."""
+    plateau = max(p["resident_GBps"] for p in pts)
+    disp = next(p for p in pts if p["resident_GBps"] >= 0.5 * plateau)
+    mall = None
+    for i in range(len(pts)):
+        if all(q["resident_same_buffer_GBps"] <= 1.02 * q["resident_GBps"] for q in pts[i:]):
+            mall = pts[i]
+            break
+    best = max(pts, key=lambda p: p["resident_same_buffer_GBps"] / p["resident_GBps"])
+    mapped = next((p for p in pts if p["mapped_GBps"] >= p["resident_GBps"]), None)
+    out = {"resident_plateau_GBps": plateau,
+           "dispatch": {"bytes": disp["bytes"], "N": disp["N"], "resident_GBps": disp["resident_GBps"],
+                        "paper_context": "about 23 MB on the paper's machine (Sec. 3.4); context, not a target"},
+           "mall": None if mall is None else {"bytes": mall["bytes"], "N": mall["N"]},
+           "largest_repeat_gain": {"bytes": best["bytes"],
+                                   "same_buffer_over_rotated": best["resident_same_buffer_GBps"] / best["resident_GBps"]},
+           "mapped_equals_resident": None if mapped is None else {"bytes": mapped["bytes"], "N": mapped["N"]}}
+    mall_txt = "none" if mall is None else f"{mall['bytes'] / 1e6:.1f} MB"
+    mapped_txt = "never" if mapped is None else f"{mapped['bytes'] / 1e6:.1f} MB"
+    log(f"size sweep: plateau {plateau:.0f} GB/s; dispatch crossover {disp['bytes'] / 1e6:.1f} MB; "
+        f"MALL crossover {mall_txt}; mapped = resident: {mapped_txt}")
     return out
 
 
