@@ -99,12 +99,12 @@ __device__ __forceinline__ u32x4 transpose_groups(u32x4 w) {
     return u32x4{s01[0], s01[1], s23[0], s23[1]};
 }
 
-/* 16-bit weights arrive as whole 128-byte lines.  Load h of a tile's half b (rows 8 b .. 8 b + 7)
-   gives lane (g, c) row 8 b + c % 8 of the tile at bytes 128 h + 16 (g + 4 (c / 8)) of the step, so
-   eight lanes cover each line.  Moving the upper eight lanes of every 16-lane row of half 0 into
-   the lower eight of half 1 and back (row shifts by 8; a lane whose source falls outside its row
-   keeps its own value) leaves lane (g, c) with row c at bytes 128 h + 16 g in the first register
-   and 128 h + 64 + 16 g in the second: the operand layout of slabs 2 h and 2 h + 1. */
+/* Weights arrive as whole 128-byte lines.  The load of a tile's half b (rows 8 b .. 8 b + 7) gives
+   lane (g, c) row 8 b + c % 8 of the tile at byte 16 (g + 4 (c / 8)) of the step's line, so eight
+   lanes cover each line.  Moving the upper eight lanes of every 16-lane row of half 0 into the
+   lower eight of half 1 and back (row shifts by 8; a lane whose source falls outside its row keeps
+   its own value) leaves lane (g, c) with row c at byte 16 g of the line in the first register and
+   at byte 64 + 16 g in the second: chunks 0 and 1 of the matrix instructions' layout. */
 __device__ __forceinline__ void lines_to_slabs(u32x4& a, u32x4& b) {
     constexpr int ROW_SHL8 = 0x108, ROW_SHR8 = 0x118;
     u32x4 lo, hi;
@@ -117,15 +117,14 @@ __device__ __forceinline__ void lines_to_slabs(u32x4& a, u32x4& b) {
     b = hi;
 }
 
-/* One step of the matrix-core loops.  Each lane reads J 16-byte chunks of its row per tile, chunk
-   jj of lane group g at byte 64 jj + 16 g of the step, so a load instruction covers 64 contiguous
-   bytes of each of 16 rows and a step 64 J bytes of every row.  With LINES the chunks are loaded
-   as whole 128-byte lines instead and put into that layout by lines_to_slabs.  HBM delivers about half its rate
-   when a wave reads only 64 bytes of a row per step, so q4 and int8 take two chunks.  SLABS is the
-   number of matrix instructions per tile and step, K the weights per row and step. */
-template <int FMT> struct MmaStep { static constexpr int J = 4, SLABS = 4, K = 128; static constexpr bool LINES = true; };   /* 8 per chunk  */
-template <> struct MmaStep<FMT_Q4> { static constexpr int J = 2, SLABS = 8, K = 256; static constexpr bool LINES = true; };  /* 32 per chunk */
-template <> struct MmaStep<FMT_I8> { static constexpr int J = 2, SLABS = 4, K = 128; static constexpr bool LINES = true; };  /* 16 per chunk */
+/* One step of the matrix-core loops: 128 bytes of every row.  The matrix instructions want chunk jj
+   (jj = 0, 1) of lane group g at byte 64 jj + 16 g of the step, 64 bytes of each of 16 rows per
+   register; the loads read the step as whole 128-byte lines, two per tile, and lines_to_slabs puts
+   them in that layout (HBM delivers about half its rate to loads of 64 bytes of each of 16 rows).
+   SLABS is the number of matrix instructions per tile and step, K the weights per row and step. */
+template <int FMT> struct MmaStep { static constexpr int J = 2, SLABS = 2, K = 64; };     /* 8 per chunk   */
+template <> struct MmaStep<FMT_Q4> { static constexpr int J = 2, SLABS = 8, K = 256; };   /* 32 per chunk  */
+template <> struct MmaStep<FMT_I8> { static constexpr int J = 2, SLABS = 4, K = 128; };   /* 16 per chunk  */
 
 /* Registers of one unit (a group of NT tiles, one step): the activations of each slab, the chunks
    of each tile, and the scales (q4: the step's eight block scales of each tile's row, as fp16
@@ -210,10 +209,9 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
     int32_t kl = 0, kc = 0;                                      /* and its step                             */
     rsrc_t rw = buffer_of(d.w), rs = buffer_of(d.w);             /* this group's row r0 of codes, scales */
     uint32_t vr[NT], vs[NT];                                     /* lane offsets: row of each tile */
-    constexpr bool LINES = MmaStep<FMT>::LINES;                  /* whole-line loads, see lines_to_slabs */
-    uint32_t vh[NT];                                             /* LINES: the row of the tile's second half */
-    const uint32_t lc = LINES ? 16 * (g + 4 * (c >> 3)) : 16 * g;   /* the lane's byte within a 64 / 128 B run */
-    static_assert(!LINES || J % 2 == 0, "line loads come in pairs of tile halves");
+    uint32_t vh[NT];                                             /* the row of the tile's second half */
+    const uint32_t lc = 16 * (g + 4 * (c >> 3));                 /* the lane's byte within a 128-byte line */
+    static_assert(J == 2, "a step is one line of each row");
     auto load = [&](Unit& u) {
         if (kl == 0) {
             const int64_t i0 = r0 + gl * 16 * NT;
@@ -224,12 +222,8 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
             for (int t = 0; t < NT; ++t) {
                 const int64_t rr = std::min<int64_t>(i0 + 16 * t + c, r1 - 1) - i0;   /* the row lane c multiplies */
                 vs[t] = (uint32_t)(rr * srow);
-                if constexpr (LINES) {
-                    vr[t] = (uint32_t)((std::min<int64_t>(i0 + 16 * t + (c & 7), r1 - 1) - i0) * crb);
-                    vh[t] = (uint32_t)((std::min<int64_t>(i0 + 16 * t + 8 + (c & 7), r1 - 1) - i0) * crb);
-                } else {
-                    vr[t] = (uint32_t)(rr * crb);
-                }
+                vr[t] = (uint32_t)((std::min<int64_t>(i0 + 16 * t + (c & 7), r1 - 1) - i0) * crb);
+                vh[t] = (uint32_t)((std::min<int64_t>(i0 + 16 * t + 8 + (c & 7), r1 - 1) - i0) * crb);
             }
         }
         if constexpr (!SHORT) {
@@ -239,9 +233,7 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
 #pragma unroll
             for (int t = 0; t < NT; ++t)
 #pragma unroll
-                for (int jj = 0; jj < J; ++jj)
-                    u.w[t][jj] = LINES ? buf_once(rw, (jj & 1 ? vh[t] : vr[t]) + lc + 128 * (jj >> 1), kb)
-                                       : buf_once(rw, vr[t] + lc + 64 * jj, kb);
+                for (int jj = 0; jj < J; ++jj) u.w[t][jj] = buf_once(rw, (jj ? vh[t] : vr[t]) + lc, kb);
 #pragma unroll
             for (int s = 0; s < SL; ++s) u.x[s] = buf_reused(rx, vx + mma_x_byte<FMT>(s), xo);
         } else {                                                 /* one step, shorter than SB: clamp per lane */
@@ -249,8 +241,7 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
             for (int t = 0; t < NT; ++t)
 #pragma unroll
                 for (int jj = 0; jj < J; ++jj)
-                    u.w[t][jj] = LINES ? buf_once(rw, (jj & 1 ? vh[t] : vr[t]) + (uint32_t)std::min<int64_t>(128 * (jj >> 1) + lc, crb - 16), 0)
-                                       : buf_once(rw, vr[t] + (uint32_t)std::min<int64_t>(64 * jj + lc, crb - 16), 0);
+                    u.w[t][jj] = buf_once(rw, (jj ? vh[t] : vr[t]) + (uint32_t)std::min<int64_t>(lc, crb - 16), 0);
 #pragma unroll
             for (int s = 0; s < SL; ++s) {
                 const int64_t e = std::min<int64_t>((XG * g + mma_x_byte<FMT>(s)) / 2, kelem - 8);
@@ -281,12 +272,8 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
         const int64_t i0 = r0 + gc * 16 * NT;
         /* the step's first weight, and the first one it has not already covered */
         const int64_t e0 = SHORT ? 0 : std::min<int64_t>((int64_t)kc * SK, kelem - SK), e1 = SHORT ? 0 : (int64_t)kc * SK;
-        if constexpr (LINES) {
 #pragma unroll
-            for (int t = 0; t < NT; ++t)
-#pragma unroll
-                for (int jj = 0; jj < J; jj += 2) lines_to_slabs(u.w[t][jj], u.w[t][jj + 1]);
-        }
+        for (int t = 0; t < NT; ++t) lines_to_slabs(u.w[t][0], u.w[t][1]);
         if (__builtin_expect(SHORT || e0 < e1, 0)) {             /* a moved-back or short last step */
             __asm__ volatile("" ::: "memory");                   /* kept a branch, not selects run every step */
 #pragma unroll
@@ -394,7 +381,7 @@ __device__ __forceinline__ void stream_range_mma(const DevMat* __restrict__ tab,
             rr.r1 = rr.r1 > f ? rr.r1 : f;
         }
         if (rr.r0 >= rr.r1) continue;
-        const bool short_rows = d.nc * 16 < 64 * (fmt == FMT_Q4 || fmt == FMT_I8 ? 2 : 4);   /* under one step */
+        const bool short_rows = d.nc * 16 < 128;                 /* under one step */
 #define WSR_ROWS(F, S16, SH) rows_mma<F, NT, S16, SH>(d, rr.r0, rr.r1, token0, ntok, lane)
         if ((FMT == 0 || FMT == FMT_F16) && fmt == FMT_F16) {
             if (short_rows) WSR_ROWS(FMT_F16, false, true); else WSR_ROWS(FMT_F16, false, false);

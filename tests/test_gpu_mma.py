@@ -142,9 +142,11 @@ def test_mma_full_size(name):
     torch.cuda.empty_cache()
 
 
-# rows shorter than one step of K (one clamped step), and a q4 shape whose scales load 8 at a time
-SHORT = [(wl.F16, 33, 40), (wl.BF16, 20, 120), (wl.Q4, 40, 96), (wl.I8, 50, 48), (wl.I8, 17, 16),
-         (wl.Q4, 70, 4096)]
+# rows shorter than one step of K (one clamped step: a step is 64 weights of 16-bit rows, 128 of
+# int8, 256 of q4), a 16-bit row one step plus a moved-back partial one, and a q4 shape whose
+# scales load 8 at a time
+SHORT = [(wl.F16, 33, 40), (wl.BF16, 20, 56), (wl.F16, 9, 8), (wl.BF16, 20, 120), (wl.Q4, 40, 96),
+         (wl.I8, 50, 48), (wl.I8, 17, 16), (wl.Q4, 70, 4096)]
 
 
 @pytest.mark.parametrize("fmt,M,K", SHORT, ids=lambda v: str(v))
