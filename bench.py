@@ -79,8 +79,6 @@ def parse():
     p.add_argument("--rows", default="probe,gemv_f16,llama8b_q4,protocol,endpoints,ordering,size_sweep,bus",
                    help="comma list of extra rows ('' for none)")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--settle-seconds", type=float, default=30.0,
-                   help="idle time between generating the headline's weights and its warm-up")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time of the sample")
     p.add_argument("--passes", type=int, default=4, help="extra timed passes for the spread")
     p.add_argument("--processes", type=int, default=0,
@@ -141,21 +139,13 @@ def spread(ms, boot=2000, seed=0):
             "ci95_median": [round(float(np.percentile(meds, 2.5)), 4), round(float(np.percentile(meds, 97.5)), 4)]}
 
 
-def run_sweep(name, steps, warmup, stream, wsr, want_cpu, cpu_seconds, passes=4, warm_seconds=0.0,
-              settle_seconds=0.0):
+def run_sweep(name, steps, warmup, stream, wsr, want_cpu, cpu_seconds, passes=4, warm_seconds=0.0):
     """warmup untimed tokens; with warm_seconds > 0 (rows other than the headline) the untimed
     sweeps go on until that much time has passed, so that a short sweep is not timed while the
-    GPU's clocks still rise after the host-side checks of the previous row.  settle_seconds of
-    idle GPU precede the warm-up (the headline): right after about a minute of other GPU jobs
-    (a test suite) the 70B sweep ran 3-4 % slower until the GPU had idled for about 30 s, while
-    90 s of back-to-back sweeps alone held their rate, so the idle keeps a previous job's
-    after-effects out of the timed region without timing a burst."""
+    GPU's clocks still rise after the host-side checks of the previous row."""
     import torch
     from synth import workloads as wl
     shape, fmt, mats, inp, specs, ws = sweep_workload(name, max(steps, warmup, 1), stream, wsr)
-    if settle_seconds > 0:
-        torch.cuda.synchronize()
-        time.sleep(settle_seconds)
     bpt = inp.weight_bytes()
     assert bpt == wl.bytes_per_token(shape, fmt)
     t0, warmed = time.perf_counter(), 0
@@ -804,7 +794,7 @@ def main():
     t_start = time.time()
 
     head = run_sweep(args.workload, args.steps, args.warmup, stream, wsr, not args.no_cpu_baseline,
-                     args.cpu_seconds, args.passes, settle_seconds=args.settle_seconds)
+                     args.cpu_seconds, args.passes)
     rows = {}
     for r in [r for r in args.rows.split(",") if r]:
         if r == "probe":
@@ -836,7 +826,6 @@ def main():
         "metric": "achieved GB/s (% of HBM peak) for decode-step GEMV sweep; tokens/s at batch 1",
         "value": round(gbps, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(head["ms_per_token"], 4), "higher_is_better": True, "scaling": "weak",
-        "settle_s": args.settle_seconds,
         "vs_baseline": None, "dtype": dtype, "data": "synthetic",
         "config": {"workload": {"llama70b_bf16": "Llama-70B-shaped bf16 decode weight sweep, batch 1",
                                 "llama8b_q4": "Llama-3-8B-shaped q4 decode weight sweep, batch 1"}[args.workload],
