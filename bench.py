@@ -120,7 +120,7 @@ def sweep_workload(name, tokens_needed, stream, wsr, check_rows=16):
     fmt = SWEEPS[name][1]
     mats = wl.decode_matrices(shape)
     t0 = time.time()
-    inp = dv.SweepInputs(mats, [fmt] * len(mats), tokens=tokens_needed)
+    inp = dv.SweepInputs(mats, [fmt] * len(mats), tokens=tokens_needed, arena=True)
     log(f"{name}: {len(mats)} matrices, {inp.weight_bytes() / 1e9:.2f} GB generated and resident "
         f"in {time.time() - t0:.1f} s")
     specs = wsr.make_mats(inp.specs())

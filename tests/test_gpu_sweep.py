@@ -53,6 +53,19 @@ def test_sweep_mixed_parity(mixed):
             assert rel_l2(ys[i][t], oracle_y(mixed, i, t)) <= TOL, (i, t)
 
 
+def test_sweep_arena_layout_bitwise_identical(mixed):
+    """Weights and scales as views into one device buffer (the benchmark's layout) give the same
+    outputs, bit for bit, as one allocation per tensor; int8 matrices included."""
+    mats = list(mixed.mats)
+    fmts = [(wl.Q4, wl.BF16, wl.I8, wl.F16)[m.layer] for m in mats]
+    own = dv.SweepInputs(mats, fmts, tokens=3)
+    one = dv.SweepInputs(mats, fmts, tokens=3, arena=True)
+    assert all(w.data_ptr() % (2 << 20) == 0 for w in one.w)
+    assert one.w[0].data_ptr() == one.arena.data_ptr()
+    for a, b in zip(run_sweep(own, 3), run_sweep(one, 3)):
+        assert np.array_equal(f32_bits(a), f32_bits(b))
+
+
 def test_sweep_paths_bitwise_identical(mixed):
     fused = run_sweep(mixed, 3)
     chained = run_sweep(mixed, 3, chained=True)
