@@ -64,23 +64,35 @@ def _run(cmd):
 KERNEL_FILES = ("wsr_kernels.hip", "wsr_mma.hip")
 
 
+def _compile_kernels(src: str) -> str:
+    obj = os.path.join(OUT_DIR, src.replace(".hip", ".o"))
+    r = _run(["hipcc", *COMMON, *DEVICE, *_MIR_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+    if "IR Dump Before" not in r.stderr:
+        raise RuntimeError(f"build: the compiler printed no machine code for the peephole check ({src})")
+    dropped = dropped_live_scc(r.stderr)
+    if dropped:
+        raise RuntimeError(f"build: the pre-emit peephole removed live SCC definitions in {src} "
+                           "(miscompiled selects):\n  " + "\n  ".join(dropped))
+    return obj
+
+
+def _compile_api() -> str:
+    obj = os.path.join(OUT_DIR, "wsr_api.o")
+    _run(["hipcc", *COMMON, "-c", os.path.join(CSRC, "wsr_api.cpp"), "-o", obj])
+    return obj
+
+
 def build(verbose: bool = False) -> str:
+    """Compile the kernel files and the C ABI (each its own hipcc process, run side by side), then
+    link libwsr.so and move it into place in one rename."""
+    from concurrent.futures import ThreadPoolExecutor
     os.makedirs(OUT_DIR, exist_ok=True)
-    objs = []
-    for src in KERNEL_FILES:
-        obj = os.path.join(OUT_DIR, src.replace(".hip", ".o"))
-        r = _run(["hipcc", *COMMON, *DEVICE, *_MIR_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
-        if "IR Dump Before" not in r.stderr:
-            raise RuntimeError(f"build: the compiler printed no machine code for the peephole check ({src})")
-        dropped = dropped_live_scc(r.stderr)
-        if dropped:
-            raise RuntimeError(f"build: the pre-emit peephole removed live SCC definitions in {src} "
-                               "(miscompiled selects):\n  " + "\n  ".join(dropped))
-        objs.append(obj)
-    a_obj = os.path.join(OUT_DIR, "wsr_api.o")
-    _run(["hipcc", *COMMON, "-c", os.path.join(CSRC, "wsr_api.cpp"), "-o", a_obj])
+    with ThreadPoolExecutor(len(KERNEL_FILES) + 1) as ex:
+        futs = [ex.submit(_compile_kernels, src) for src in KERNEL_FILES]
+        api = ex.submit(_compile_api)
+        objs = [f.result() for f in futs] + [api.result()]
     tmp = LIB_PATH + ".tmp"
-    _run(["hipcc", "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, a_obj, "-o", tmp])
+    _run(["hipcc", "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp])
     os.replace(tmp, LIB_PATH)
     if verbose:
         print("built", LIB_PATH)
