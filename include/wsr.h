@@ -74,7 +74,9 @@ int wsr_abi_version(void);
    alias a neighbouring tensor); one call yields one registration and nothing is cached by address
    (WSR_E_STATE if [host] is already registered).
    - A range already device-visible (pinned host memory from hipHostMalloc, e.g. a PyTorch pinned
-     tensor) is adopted in place: no copy and no new pin; *granted_out gets WSR_REG_PREPINNED.
+     tensor) is adopted in place: no copy and no new pin; *granted_out gets WSR_REG_PREPINNED.  The
+     whole range must lie inside that one pinned allocation (WSR_E_SIZE if it runs past its end;
+     WSR_E_UNSUPPORTED if the runtime does not report the allocation's extent).
    - Any other range is pinned with hipHostRegister only if `flags` has WSR_REG_PIN; with
      WSR_REG_READONLY as well, a read-only pin is requested first (Sec. 5.1, read-only intent) and
      *granted_out reports WSR_REG_READONLY if it was granted.  A refused pin returns

@@ -100,6 +100,40 @@ DevMat make_devmat(int fmt, int64_t M, int64_t K, const void* w, const void* sca
     return d;
 }
 
+/* [p, p + bytes) lies inside [start, start + size). */
+bool inside(const void* p, size_t bytes, const void* start, size_t size) {
+    const uintptr_t a = reinterpret_cast<uintptr_t>(p), s0 = reinterpret_cast<uintptr_t>(start);
+    return a >= s0 && a - s0 <= size && bytes <= size - (a - s0);
+}
+
+/* The extent of the pinned allocation that holds `host` (device view `dev`) must cover the whole
+ * requested range.  The runtime is asked for the allocation's range through the host address and,
+ * if that gives no answer, through the device address; a range it cannot bound is refused. */
+wsr_status check_pinned_extent(const void* host, const void* dev, size_t bytes) {
+    void* start = nullptr;
+    size_t size = 0;
+    hipDeviceptr_t hp = const_cast<void*>(host);
+    if (hipPointerGetAttribute(&start, HIP_POINTER_ATTRIBUTE_RANGE_START_ADDR, hp) == hipSuccess &&
+        hipPointerGetAttribute(&size, HIP_POINTER_ATTRIBUTE_RANGE_SIZE, hp) == hipSuccess && size > 0 &&
+        inside(host, 1, start, size)) {
+        if (inside(host, bytes, start, size)) return WSR_OK;
+        return fail(WSR_E_SIZE, "register_host: %p + %zu runs past the end of its pinned allocation "
+                    "(%p + %zu)", host, bytes, start, size);
+    }
+    (void)hipGetLastError();
+    hipDeviceptr_t base = nullptr;
+    size = 0;
+    if (hipMemGetAddressRange(&base, &size, const_cast<void*>(dev)) == hipSuccess && size > 0 &&
+        inside(dev, 1, base, size)) {
+        if (inside(dev, bytes, base, size)) return WSR_OK;
+        return fail(WSR_E_SIZE, "register_host: %p + %zu runs past the end of its pinned allocation "
+                    "(device range %p + %zu)", host, bytes, base, size);
+    }
+    (void)hipGetLastError();
+    return fail(WSR_E_UNSUPPORTED, "register_host: the runtime does not report the extent of the pinned "
+                "allocation holding %p, so the range cannot be checked", host);
+}
+
 }  // namespace
 
 extern "C" {
@@ -129,7 +163,11 @@ wsr_status wsr_register_host(const void* host, size_t bytes, unsigned flags, con
     hipPointerAttribute_t attr{};
     const hipError_t qa = hipPointerGetAttributes(&attr, host);
     if (qa == hipSuccess && attr.type == hipMemoryTypeHost && attr.devicePointer != nullptr) {
-        dev = attr.devicePointer;               /* already pinned and mapped: adopt in place */
+        /* Already pinned and mapped: adopt in place, but only if the whole range lies inside that
+         * one pinned allocation; pages past its end are not device-visible. */
+        const wsr_status st = check_pinned_extent(host, attr.devicePointer, bytes);
+        if (st != WSR_OK) return st;
+        dev = attr.devicePointer;
         granted |= WSR_REG_PREPINNED;
     } else {
         (void)hipGetLastError();                /* an unknown pointer is not an error here */

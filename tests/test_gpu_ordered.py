@@ -5,9 +5,10 @@ import numpy as np
 import pytest
 import torch
 
+import oracle
 from synth import device as dv
 from synth import workloads as wl
-from gpu_util import f32_bits, needs_gpu, stream, zeros_u8
+from gpu_util import TOL, f32_bits, needs_gpu, rel_l2, stream, zeros_u8
 
 from paper_2608_12114_amd import wsr
 
@@ -22,6 +23,17 @@ def model():
     return dv.SweepInputs(mats, fmts, tokens=1)
 
 
+@pytest.fixture(scope="module")
+def want_oracle(model):
+    """The oracle's outputs of the pass, one vector per matrix."""
+    ora, out = oracle.get(), []
+    for i, fmt in enumerate(model.fmts):
+        hw, x = model.host_weights(i), model.host_x(i, 0)
+        out.append(ora.gemv(dict(fmt=fmt, w=hw[0], s=hw[1]), x, threads=8) if fmt in (wl.Q4, wl.I8)
+                   else ora.gemv16(hw, x, fmt, threads=8))
+    return out
+
+
 def plain(inp):
     for y in inp.y:
         y.fill_(float("nan"))
@@ -33,7 +45,7 @@ def plain(inp):
 
 
 @pytest.mark.parametrize("mode", MODES, ids=lambda m: wsr.ORDER_NAMES[m].replace(" ", "_"))
-def test_ordered_pass_sees_and_is_seen(model, mode):
+def test_ordered_pass_sees_and_is_seen(model, want_oracle, mode):
     want = plain(model)
     xs = list(model.x.values())
     saved = [x[0].clone() for x, _ in xs]
@@ -58,6 +70,8 @@ def test_ordered_pass_sees_and_is_seen(model, mode):
         seen = [y.clone() for y in model.y]
     torch.cuda.synchronize()
     for i, (w, y, c) in enumerate(zip(want, model.y, seen)):
-        assert np.array_equal(f32_bits(w.cpu().numpy()), f32_bits(y.cpu().numpy())), (wsr.ORDER_NAMES[mode], i)
+        got = y.cpu().numpy()
+        assert rel_l2(got[0], want_oracle[i]) <= TOL, (wsr.ORDER_NAMES[mode], i)
+        assert np.array_equal(f32_bits(w.cpu().numpy()), f32_bits(got)), (wsr.ORDER_NAMES[mode], i)
         assert np.array_equal(f32_bits(w.cpu().numpy()), f32_bits(c.cpu().numpy())), (wsr.ORDER_NAMES[mode], i)
     del b
