@@ -225,7 +225,7 @@ def _oracle_rows(inp, i, t, rows):
     return np.array(out)
 
 
-@pytest.mark.parametrize("batch", [None, 2, 3], ids=["sweep", "batched2", "batched3"])
+@pytest.mark.parametrize("batch", [None, 2, 4], ids=["sweep", "batched2", "batched4"])
 def test_sweep_host_mapped(mapped_model, batch):
     """wsr_decode_sweep / wsr_decode_sweep_batched with every weight and scale read in place from
     registered host memory: every output of the small model against the oracle (all tokens), the

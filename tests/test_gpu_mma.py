@@ -18,6 +18,10 @@ pytestmark = [pytest.mark.gpu, needs_gpu]
 CODE = {wl.F16: wsr.WSR_F16, wl.BF16: wsr.WSR_BF16, wl.Q4: wsr.WSR_Q4, wl.I8: wsr.WSR_I8}
 # K past a whole number of steps (128 elements; 64 for int8) and M past whole 64-row groups
 SHAPES = {wl.F16: (100, 520), wl.BF16: (77, 4104), wl.Q4: (100, 2080), wl.I8: (130, 2064)}
+# Matrix-core against vector-ALU outputs: both form every product exactly and sum in fp32, in
+# different orders, so they differ by fp32 rounding only (worst measured on these seeded inputs:
+# 7.0e-6 rel-L2, the 8B q4 down projection with K = 14336; 1e-6 or less for 16-bit and int8).
+MMA_VS_VALU = 1e-5
 
 
 def host_matrix(fmt, M, K, seed):
@@ -106,7 +110,7 @@ def test_mma_mixed_sweep(chained):
     for i, (m, fmt) in enumerate(zip(mats, fmts)):
         a, b = valu[i].cpu().numpy(), mma[i].cpu().numpy()
         for t in range(19):
-            assert rel_l2(b[t], a[t]) <= 5e-5, (m.name, m.layer, t)   # summation order only
+            assert rel_l2(b[t], a[t]) <= MMA_VS_VALU, (m.name, m.layer, t)
         for t in (0, 15, 16, 18):
             hw = inp.host_weights(i)
             x = inp.host_x(i, t)
@@ -127,7 +131,7 @@ def test_mma_full_size(name):
     valu, mma = sweep_pair(inp, 16)
     ora = oracle.get()
     for i, m in enumerate(mats):
-        assert rel_l2(mma[i].cpu().numpy(), valu[i].cpu().numpy()) <= 5e-5, (m.name, m.layer)
+        assert rel_l2(mma[i].cpu().numpy(), valu[i].cpu().numpy()) <= MMA_VS_VALU, (m.name, m.layer)
         rows = np.unique(np.linspace(0, m.M - 1, 4).astype(np.int64))
         for t in (0, 15):
             x = inp.host_x(i, t)
@@ -226,7 +230,7 @@ def test_mma_mixed_full_size_tail():
     valu, mma = sweep_pair(inp, 16)
     ora = oracle.get()
     for i, (m, fmt) in enumerate(zip(mats, fmts)):
-        assert rel_l2(mma[i].cpu().numpy(), valu[i].cpu().numpy()) <= 5e-5, (m.name, fmt)
+        assert rel_l2(mma[i].cpu().numpy(), valu[i].cpu().numpy()) <= MMA_VS_VALU, (m.name, fmt)
         rows = np.unique(np.linspace(0, m.M - 1, 4).astype(np.int64))
         for t in (0, 15):
             x = inp.host_x(i, t)
