@@ -198,6 +198,22 @@ wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, vo
 wsr_status wsr_decode_sweep_batched(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch,
                                     void* ws, size_t ws_bytes, void* stream);
 
+/* ---- the decode sweep without a workspace ------------------------------------------------------
+
+   wsr_decode_sweep_noalloc: for callers that cannot allocate device memory (code under HIP graph
+   capture, tight serving loops, harnesses that forbid hipMalloc).  The outputs of
+   wsr_decode_sweep(mats, n, n_tokens, ws, ws_bytes, stream), bit for bit (the same kernels), with
+   the workspace taken from the library's own scratch: a device array of 512 KiB per GPU, which
+   holds the table of up to about 5,000 matrices (wsr_sweep_workspace_bytes(mats, n) <= 524288,
+   else WSR_E_SIZE; a 70B-shaped model has 561).  The call allocates and frees nothing.  The first
+   call on a device looks up that device's scratch address (a HIP query, no allocation); the
+   scratch stays with the device until the process ends.  Every call on one GPU shares that GPU's
+   scratch, and each call rewrites it before use (table and counters; nothing carries over).
+   Calls enqueued on one stream run one after another; calls whose work overlaps on one GPU (on
+   different streams, or from several threads with no ordering between them) race on the scratch
+   and must not be made. */
+wsr_status wsr_decode_sweep_noalloc(const wsr_mat* mats, int32_t n, int32_t n_tokens, void* stream);
+
 /* ---- batched decode on the matrix cores (Sec. 3.4, 5.2: several activation columns per weight read) -
 
    wsr_decode_sweep_mma: for t < n_tokens and every matrix m, y_m(t) = W_m . x_m(t) as in

@@ -360,7 +360,9 @@ struct SweepPlan {
     int32_t batch = 1;
 };
 
-/* Every check of a sweep; enqueues nothing. */
+wsr_status plan_table(const wsr_mat* mats, int32_t n, int32_t batch, int32_t n_tokens, SweepPlan& p);
+
+/* Every check of a sweep with a caller's workspace; enqueues nothing. */
 wsr_status plan_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch, void* ws,
                       size_t ws_bytes, SweepPlan& p) {
     if (n < 0 || n_tokens < 1) return fail(WSR_E_ARG, "decode_sweep: n=%d n_tokens=%d", n, n_tokens);
@@ -371,7 +373,11 @@ wsr_status plan_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t 
     if (!aligned(ws, 256)) return fail(WSR_E_ALIGN, "decode_sweep: workspace must be 256-byte aligned");
     const size_t need = wsr_sweep_workspace_bytes(mats, n);
     if (ws_bytes < need) return fail(WSR_E_SIZE, "decode_sweep: workspace %zu < %zu bytes", ws_bytes, need);
+    return plan_table(mats, n, batch, n_tokens, p);
+}
 
+/* The per-matrix checks and the device table of a sweep (n > 0, mats not null). */
+wsr_status plan_table(const wsr_mat* mats, int32_t n, int32_t batch, int32_t n_tokens, SweepPlan& p) {
     p.tab.assign((size_t)n, DevMat{});
     p.segs.clear();
     char who[64];
@@ -449,6 +455,26 @@ wsr_status wsr_decode_sweep(const wsr_mat* mats, int32_t n, int32_t n_tokens, vo
 wsr_status wsr_decode_sweep_batched(const wsr_mat* mats, int32_t n, int32_t n_tokens, int32_t batch,
                                     void* ws, size_t ws_bytes, void* stream) {
     return sweep(mats, n, n_tokens, batch, ws, ws_bytes, stream);
+}
+
+/* wsr_decode_sweep with the library's own per-device scratch as its workspace: no allocation and
+   no workspace argument.  Every argument check runs before the scratch is looked up. */
+wsr_status wsr_decode_sweep_noalloc(const wsr_mat* mats, int32_t n, int32_t n_tokens, void* stream) {
+    if (n < 0 || n_tokens < 1) return fail(WSR_E_ARG, "decode_sweep_noalloc: n=%d n_tokens=%d", n, n_tokens);
+    if (n == 0) return ok();
+    if (!mats) return fail(WSR_E_ARG, "decode_sweep_noalloc: null pointer");
+    const size_t need = wsr_sweep_workspace_bytes(mats, n);
+    if (need > wsr::NOALLOC_SCRATCH_BYTES)
+        return fail(WSR_E_SIZE, "decode_sweep_noalloc: a table of %d matrices needs %zu bytes of scratch; "
+                    "the library holds %zu (pass a workspace to wsr_decode_sweep instead)", n, need,
+                    wsr::NOALLOC_SCRATCH_BYTES);
+    SweepPlan p;
+    wsr_status st = plan_table(mats, n, 1, n_tokens, p);
+    if (st != WSR_OK) return st;
+    void* ws = nullptr;
+    const hipError_t e = wsr::noalloc_scratch(&ws);
+    if (e != hipSuccess) return hip_fail(e, "decode_sweep_noalloc: scratch address");
+    return run_sweep(p, n, n_tokens, ws, stream);
 }
 
 }  // extern "C"

@@ -51,6 +51,13 @@ hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, int nmat, int64_
    stream offsets (DevMat::cost0) as a dense int64 array, each part padded to 256 bytes. */
 constexpr size_t SWEEP_CTR_BYTES = 256;
 
+/* The library's own sweep workspace for callers that cannot allocate device memory: a file-scope
+   device array of NOALLOC_SCRATCH_BYTES per device (a table of up to about 5,000 matrices).
+   noalloc_scratch returns its address on the current device; the first call on a device looks it
+   up (hipGetSymbolAddress) and later calls reuse that address. */
+constexpr size_t NOALLOC_SCRATCH_BYTES = 512 << 10;
+hipError_t noalloc_scratch(void** ptr);
+
 }  // namespace wsr
 
 #endif

@@ -18,6 +18,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "wsr_device.h"
 
@@ -429,6 +430,33 @@ hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, int nmat, int64_
         default:   /* mixed formats; a table holding q4 or int8 comes with T <= 8 */
             return launch_sweep_cols<0>(grid, T, s, tab, cost, nmat, total, tile, token, ctr);
     }
+}
+
+/* ================================ allocation-free sweep scratch ================================ */
+
+/* Each device holds its own copy of this array, at its own address, from the time the library's
+   code is loaded on that device until the process ends.  Host code never passes the array's name
+   to a kernel or a copy: that name is a host-side stand-in, not a device address.  It uses the
+   address hipGetSymbolAddress reports for the current device, looked up once per device. */
+static __device__ __align__(256) unsigned char scratch[NOALLOC_SCRATCH_BYTES];
+
+hipError_t noalloc_scratch(void** ptr) {
+    static std::mutex mu;
+    static void* addr[64] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(mu);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
 }
 
 }  // namespace wsr

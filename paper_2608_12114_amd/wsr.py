@@ -81,10 +81,11 @@ _L.wsr_host_resident_pages.argtypes = [_vp, _sz, ctypes.POINTER(_sz), ctypes.POI
 _L.wsr_select_endpoint.argtypes = [ctypes.POINTER(wsr_endpoint_probe), ctypes.c_double, ctypes.POINTER(_i32),
                                    ctypes.POINTER(ctypes.c_double)]
 _L.wsr_gemv_i8_cols.argtypes = [_vp, _vp, _vp, _i64, _vp, _i64, _i64, _i64, _i32, _vp]
+_L.wsr_decode_sweep_noalloc.argtypes = [ctypes.POINTER(wsr_mat), _i32, _i32, _vp]
 for _f in ("wsr_register_host", "wsr_unregister_host", "wsr_probe_read", "wsr_gemv_f16",
            "wsr_gemv_q4", "wsr_decode_sweep", "wsr_gemv_f16_cols", "wsr_decode_sweep_batched",
            "wsr_gemv_q4_cols", "wsr_gemv_i8", "wsr_gemv_i8_cols", "wsr_sweep_staged", "wsr_host_resident_pages", "wsr_decode_sweep_ordered", "wsr_decode_sweep_mma",
-           "wsr_select_endpoint"):
+           "wsr_select_endpoint", "wsr_decode_sweep_noalloc"):
     getattr(_L, _f).restype = ctypes.c_int
 
 
@@ -193,6 +194,10 @@ def wsr_sweep_workspace_bytes(mats) -> int:
 
 def wsr_decode_sweep(mats, n_tokens: int, ws, ws_bytes: int, stream=None) -> None:
     _check(_L.wsr_decode_sweep(mats, _n(mats), n_tokens, _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def wsr_decode_sweep_noalloc(mats, n_tokens: int, stream=None) -> None:
+    _check(_L.wsr_decode_sweep_noalloc(mats, _n(mats), n_tokens, _stream(stream)))
 
 
 def wsr_decode_sweep_batched(mats, n_tokens: int, batch: int, ws, ws_bytes: int, stream=None) -> None:

@@ -21,7 +21,7 @@ def declared():
 
 def test_exports_every_declared_symbol():
     names = declared()
-    assert len(names) == 20, names
+    assert len(names) == 21, names
     for n in names:
         assert hasattr(L, n), n
 
@@ -156,6 +156,25 @@ def test_sweep_argument_checks():
         m = wsr.make_mats([good, bad])
         assert _status(f, m, 2, 1, A, ws, None) == st, bad
         assert "matrix 1" in wsr.wsr_last_error()
+
+
+def test_sweep_noalloc_argument_checks():
+    """The allocation-free sweep checks its arguments, and the size of its table against the
+    library's 512 KiB scratch, before any HIP call."""
+    good = dict(fmt=2, M=8, K=64, w=A, x=A, y=A, x_tok_stride=128, y_tok_stride=32)
+    f = "wsr_decode_sweep_noalloc"
+    mats = wsr.make_mats([good, good])
+    assert _status(f, mats, 2, 0, None) == wsr.WSR_E_ARG                      # n_tokens < 1
+    assert _status(f, mats, -1, 1, None) == wsr.WSR_E_ARG
+    assert _status(f, None, 2, 1, None) == wsr.WSR_E_ARG
+    assert _status(f, mats, 0, 1, None) == wsr.WSR_OK                         # empty sweep
+    bad = wsr.make_mats([good, dict(good, K=60)])
+    assert _status(f, bad, 2, 1, None) == wsr.WSR_E_ALIGN and "matrix 1" in wsr.wsr_last_error()
+    big = wsr.make_mats([dict(good, K=60)] * 6000)     # K = 60 is misaligned: the size check comes first
+    fits = max(n for n in range(4000, 6000) if L.wsr_sweep_workspace_bytes(big, n) <= 512 << 10)
+    assert fits >= 5000
+    assert _status(f, big, fits + 1, 1, None) == wsr.WSR_E_SIZE
+    assert "scratch" in wsr.wsr_last_error()
 
 
 def test_sweep_staged_argument_checks():
