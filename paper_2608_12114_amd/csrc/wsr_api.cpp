@@ -420,14 +420,22 @@ wsr_status run_sweep(const SweepPlan& p, int32_t n, int32_t n_tokens, void* ws, 
     DevMat* dtab = reinterpret_cast<DevMat*>(static_cast<char*>(ws) + wsr::SWEEP_CTR_BYTES);
     int64_t* dcost = reinterpret_cast<int64_t*>(reinterpret_cast<char*>(dtab) +
                                                 ((size_t)n * sizeof(DevMat) + 255) / 256 * 256);
-    hipError_t e = wsr::launch_put_table(dtab, dcost, p.tab.data(), n, ctr, s);
-    if (e != hipSuccess) return hip_fail(e, "decode_sweep: table upload");
-    /* The last tokens go in passes of the largest power of two that fits. */
+    /* The last tokens go in passes of the largest power of two that fits.  The table goes to the
+       workspace only if some launch reads it there; the others carry it in their arguments. */
+    bool upload = false;
+    for (int32_t t = 0, T = p.batch; t < n_tokens && !upload; t += T) {
+        while (T > n_tokens - t) T >>= 1;
+        for (const Seg& g : p.segs) upload |= !wsr::sweep_table_by_value(g.count, g.total, g.fmt, T);
+    }
+    hipError_t e = hipSuccess;
+    if (upload && (e = wsr::launch_put_table(dtab, dcost, p.tab.data(), n, ctr, s)) != hipSuccess)
+        return hip_fail(e, "decode_sweep: table upload");
     for (int32_t t = 0; t < n_tokens;) {
         int32_t T = p.batch;
         while (T > n_tokens - t) T >>= 1;
         for (const Seg& g : p.segs) {
-            e = wsr::launch_sweep(dtab + g.first, dcost + g.first, g.count, g.total, g.fmt, t, T, ctr, s);
+            e = wsr::launch_sweep(dtab + g.first, dcost + g.first, p.tab.data() + g.first, g.count, g.total, g.fmt,
+                                  t, T, ctr, s);
             if (e != hipSuccess) return hip_fail(e, "decode_sweep: launch");
         }
         t += T;

@@ -43,9 +43,13 @@ hipError_t launch_gemv_cols(const DevMat& m, int T, hipStream_t s);
 hipError_t launch_put_table(DevMat* dst, int64_t* cost, const DevMat* src, int n, unsigned* ctr,
                             hipStream_t s);
 /* One pass over the table's weights for tokens token .. token + T - 1 (T = 1, 2, 4, 8, 16; at most
-   8 when the table holds a q4 or int8 matrix). */
-hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, int nmat, int64_t total_bytes,
+   8 when the table holds a q4 or int8 matrix).  tab / cost: the table in device memory (written by
+   launch_put_table); htab: the same table on the host, or null.  A launch for which
+   sweep_table_by_value() holds and htab is given carries the table in its arguments and reads
+   neither tab, cost nor ctr. */
+hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, const DevMat* htab, int nmat, int64_t total_bytes,
                         int fmt_all, int32_t token, int T, unsigned* ctr, hipStream_t s);
+bool sweep_table_by_value(int nmat, int64_t total_bytes, int fmt_all, int T);
 
 /* Sweep workspace: tile counters in the first SWEEP_CTR_BYTES, then the table, then the matrices'
    stream offsets (DevMat::cost0) as a dense int64 array, each part padded to 256 bytes. */

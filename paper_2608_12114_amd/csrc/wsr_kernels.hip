@@ -282,6 +282,14 @@ int64_t sweep_tile(int64_t total, int64_t waves) {
     return t;
 }
 
+/* Wave w of nw takes bytes [floor(total w / nw), floor(total (w + 1) / nw)) of the stream, computed
+   without forming total * w. */
+__device__ __forceinline__ void span_bounds(int64_t total, int64_t w, unsigned nw, int64_t& lo, int64_t& hi) {
+    const int64_t q = total / nw, r = total % nw;
+    lo = q * w + (int64_t)((uint64_t)r * (uint64_t)w / nw);
+    hi = q * (w + 1) + (int64_t)((uint64_t)r * (uint64_t)(w + 1) / nw);
+}
+
 /* Work distribution over the weight stream [0, total) of one token:
      SCHED_TILES   tiles of `tile` bytes, claimed in order from a counter;
      SCHED_SPANS   wave w takes [total w / nw, total (w + 1) / nw); with many more blocks than the
@@ -302,10 +310,8 @@ __global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab,
     const int64_t w = (int64_t)blockIdx.x * WAVES_PER_BLOCK + wave_in_block();
     int hint = 0;
     if constexpr (SCHED == SCHED_SPANS) {
-        /* floor(total w / nw) without forming total * w */
-        const int64_t q = total / nw, r = total % nw;
-        const int64_t lo = q * w + (int64_t)((uint64_t)r * (uint64_t)w / nw);
-        const int64_t hi = q * (w + 1) + (int64_t)((uint64_t)r * (uint64_t)(w + 1) / nw);
+        int64_t lo, hi;
+        span_bounds(total, w, nw, lo, hi);
         if (lo < hi) stream_range<FMT, R16, U16, RQ, UQ, QNB, T, RC, UC, RQC>(tab, cost, nmat, lo, hi, token, lane, hint);
     } else {
         int64_t base = 0;
@@ -337,6 +343,32 @@ __global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab,
     }
 }
 
+/* A table of up to N matrices carried by value in the arguments of a span-scheduled sweep launch.
+   The waves read their matrix records and stream offsets straight from the argument memory through
+   the scalar cache, so such a sweep needs neither a workspace nor the table upload launch before
+   it, whose kernel boundary measured about 4 us per call against a 1 GB pass of about 150 us.  Two
+   sizes: 32 entries (3.3 KB, about 1 us per launch cheaper than the large block on a 32-matrix
+   pass) and TABLE_ARG_MAX (29,952 bytes; arguments of up to 32,000 bytes were checked to arrive
+   intact). */
+constexpr int TABLE_ARG_SMALL = 32, TABLE_ARG_MAX = 288;
+template <int N>
+struct TableArg {
+    DevMat m[N];
+    int64_t cost[N];
+};
+static_assert(sizeof(TableArg<TABLE_ARG_MAX>) + 32 <= 32000, "the by-value table must stay within the checked argument size");
+
+template <int FMT, int R16, int U16, int T, int N>
+__global__ __launch_bounds__(BLOCK) void k_sweep_arg(TableArg<N> tb, int nmat, int64_t total, int32_t token) {
+    const int lane = threadIdx.x & (WAVE - 1);
+    const unsigned nw = gridDim.x * WAVES_PER_BLOCK;
+    const int64_t w = (int64_t)blockIdx.x * WAVES_PER_BLOCK + wave_in_block();
+    int hint = 0;
+    int64_t lo, hi;
+    span_bounds(total, w, nw, lo, hi);
+    if (lo < hi) stream_range<FMT, R16, U16, 8, 1, 2, T>(tb.m, tb.cost, nmat, lo, hi, token, lane, hint);
+}
+
 static int cu_count() {
     static int cache[64] = {0};
     int dev = 0;
@@ -359,6 +391,14 @@ static int cu_count() {
    (one wave per SIMD cannot cover the latency at each row group's start). */
 constexpr int SWEEP_BLOCKS_PER_CU_16 = 1;
 constexpr int64_t SWEEP_SPAN_Q4 = 48 << 10;
+/* 16-bit streams shorter than four tiles of the largest size per wave (8 GiB with 1024 waves) go
+   over spans of about 48 KiB per wave, two rows x 8 KiB steps, instead of claimed tiles: with few
+   tiles per wave the end of the launch is uneven (the 1 GiB pass of 32 matrices of 4096 x 4096 fp16
+   measured 4.47 TB/s over tiles and 6.8 TB/s over spans), while on long streams tiles keep the
+   waves on one moving front (the 70B bf16 token measured 7.22 TB/s over tiles, 7.10 over spans). */
+constexpr int64_t SWEEP_SPAN_16 = 48 << 10;
+constexpr int64_t SWEEP16_TILES_FROM = int64_t{8} << 30;
+constexpr int SPAN16_R = 2, SPAN16_U = 8;
 constexpr int64_t SWEEP_SPAN_I8[4] = {32 << 10, 32 << 10, 128 << 10, 128 << 10};   /* T = 1, 2, 4, 8 */
 
 /* Grid of a span-scheduled sweep: about `span` bytes per wave, at least one wave per SIMD. */
@@ -370,29 +410,61 @@ static hipError_t span_grid(int64_t total, int64_t span, dim3& g) {
     return hipSuccess;
 }
 
+template <int N>
+static void fill_table_arg(TableArg<N>& tb, const DevMat* htab, int nmat) {
+    for (int i = 0; i < nmat; ++i) {
+        tb.m[i] = htab[i];
+        tb.cost[i] = htab[i].cost0;
+    }
+}
+
+/* One span-scheduled launch: the table by value when the host table is given (nmat <= TABLE_ARG_MAX),
+   else from the device table. */
 template <int FMT, int T>
-static void launch_sweep_spans(dim3 g, hipStream_t s, const DevMat* tab, const int64_t* cost, int nmat,
-                               int64_t total, int32_t token) {
-    hipLaunchKernelGGL((k_sweep<FMT, SCHED_SPANS, 4, 4, 8, 1, 2, T>), g, dim3(BLOCK), 0, s, tab, cost, nmat, total,
-                       (int64_t)0, (int64_t)0, token, nullptr);
+static void launch_sweep_spans(dim3 g, hipStream_t s, const DevMat* tab, const int64_t* cost, const DevMat* htab,
+                               int nmat, int64_t total, int32_t token) {
+    constexpr int R = (FMT == FMT_F16 || FMT == FMT_BF16) ? SPAN16_R : 4;
+    constexpr int U = (FMT == FMT_F16 || FMT == FMT_BF16) ? SPAN16_U : 4;
+    if (htab && nmat <= TABLE_ARG_SMALL) {
+        TableArg<TABLE_ARG_SMALL> tb;
+        fill_table_arg(tb, htab, nmat);
+        hipLaunchKernelGGL((k_sweep_arg<FMT, R, U, T, TABLE_ARG_SMALL>), g, dim3(BLOCK), 0, s, tb, nmat, total, token);
+    } else if (htab) {
+        TableArg<TABLE_ARG_MAX> tb;
+        fill_table_arg(tb, htab, nmat);
+        hipLaunchKernelGGL((k_sweep_arg<FMT, R, U, T, TABLE_ARG_MAX>), g, dim3(BLOCK), 0, s, tb, nmat, total, token);
+    } else {
+        hipLaunchKernelGGL((k_sweep<FMT, SCHED_SPANS, R, U, 8, 1, 2, T>), g, dim3(BLOCK), 0, s, tab, cost, nmat,
+                           total, (int64_t)0, (int64_t)0, token, nullptr);
+    }
 }
 
 /* q4 and int8 sweeps (T <= 8) over spans. */
 template <int FMT>
-static hipError_t launch_sweep_quant(int T, hipStream_t s, const DevMat* tab, const int64_t* cost, int nmat,
-                                     int64_t total, int32_t token) {
+static hipError_t launch_sweep_quant(int T, hipStream_t s, const DevMat* tab, const int64_t* cost, const DevMat* htab,
+                                     int nmat, int64_t total, int32_t token) {
     const int ti = T == 1 ? 0 : T == 2 ? 1 : T == 4 ? 2 : 3;
     dim3 g;
     const hipError_t e = span_grid(total, FMT == FMT_Q4 ? SWEEP_SPAN_Q4 : SWEEP_SPAN_I8[ti], g);
     if (e != hipSuccess) return e;
     switch (T) {
-        case 1: launch_sweep_spans<FMT, 1>(g, s, tab, cost, nmat, total, token); break;
-        case 2: launch_sweep_spans<FMT, 2>(g, s, tab, cost, nmat, total, token); break;
-        case 4: launch_sweep_spans<FMT, 4>(g, s, tab, cost, nmat, total, token); break;
-        case 8: launch_sweep_spans<FMT, 8>(g, s, tab, cost, nmat, total, token); break;
+        case 1: launch_sweep_spans<FMT, 1>(g, s, tab, cost, htab, nmat, total, token); break;
+        case 2: launch_sweep_spans<FMT, 2>(g, s, tab, cost, htab, nmat, total, token); break;
+        case 4: launch_sweep_spans<FMT, 4>(g, s, tab, cost, htab, nmat, total, token); break;
+        case 8: launch_sweep_spans<FMT, 8>(g, s, tab, cost, htab, nmat, total, token); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
+}
+
+/* Which launches run over spans (those may take their table by value). */
+static bool sweep_spans(int64_t total, int fmt_all, int T) {
+    return fmt_all == FMT_Q4 || fmt_all == FMT_I8 ||
+           ((fmt_all == FMT_F16 || fmt_all == FMT_BF16) && T == 1 && total < SWEEP16_TILES_FROM);
+}
+
+bool sweep_table_by_value(int nmat, int64_t total, int fmt_all, int T) {
+    return nmat <= TABLE_ARG_MAX && sweep_spans(total, fmt_all, T);
 }
 
 /* 16-bit (or mixed-format) sweep over tiles, tokens token .. token + T - 1 per weight pass. */
@@ -417,11 +489,20 @@ static hipError_t launch_sweep_cols(dim3 grid, int T, hipStream_t s, const DevMa
     return hipGetLastError();
 }
 
-hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, int nmat, int64_t total, int fmt_all,
-                        int32_t token, int T, unsigned* ctr, hipStream_t s) {
+hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, const DevMat* htab, int nmat, int64_t total,
+                        int fmt_all, int32_t token, int T, unsigned* ctr, hipStream_t s) {
     if (nmat == 0 || total == 0) return hipSuccess;
-    if (fmt_all == FMT_Q4) return launch_sweep_quant<FMT_Q4>(T, s, tab, cost, nmat, total, token);
-    if (fmt_all == FMT_I8) return launch_sweep_quant<FMT_I8>(T, s, tab, cost, nmat, total, token);
+    if (!sweep_table_by_value(nmat, total, fmt_all, T)) htab = nullptr;
+    if (fmt_all == FMT_Q4) return launch_sweep_quant<FMT_Q4>(T, s, tab, cost, htab, nmat, total, token);
+    if (fmt_all == FMT_I8) return launch_sweep_quant<FMT_I8>(T, s, tab, cost, htab, nmat, total, token);
+    if (sweep_spans(total, fmt_all, T)) {
+        dim3 g;
+        const hipError_t e = span_grid(total, SWEEP_SPAN_16, g);
+        if (e != hipSuccess) return e;
+        if (fmt_all == FMT_F16) launch_sweep_spans<FMT_F16, 1>(g, s, tab, cost, htab, nmat, total, token);
+        else launch_sweep_spans<FMT_BF16, 1>(g, s, tab, cost, htab, nmat, total, token);
+        return hipGetLastError();
+    }
     const dim3 grid((unsigned)(cu_count() * SWEEP_BLOCKS_PER_CU_16));
     const int64_t tile = sweep_tile(total, (int64_t)grid.x * WAVES_PER_BLOCK);
     switch (fmt_all) {

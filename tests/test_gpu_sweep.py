@@ -138,3 +138,31 @@ def test_sweep_full_size(name):
     _check_sampled(inp, [0, 3])
     del inp
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("n", [32, 33, 288, 289])
+@pytest.mark.parametrize("fmt", [wl.BF16, wl.Q4, wl.I8])
+def test_sweep_table_sizes(n, fmt):
+    """Tables on both sides of the by-value limits of a span-scheduled sweep (up to 32 and up to 288
+    matrices carried in the launch arguments, more read from the workspace): every matrix, with
+    ragged row counts, against the oracle for both tokens and bit for bit against its standalone
+    GEMV."""
+    K = 512
+    mats = [wl.Mat(i, f"m{i}", i, 1 + (37 * i) % 70, K, "attn") for i in range(n)]
+    inp = dv.SweepInputs(mats, [fmt] * n, tokens=2)
+    ys = run_sweep(inp, 2)
+    ora = oracle.get()
+    gemv = {wl.BF16: None, wl.Q4: wsr.wsr_gemv_q4, wl.I8: wsr.wsr_gemv_i8}[fmt]
+    for i, m in enumerate(mats):
+        hw = inp.host_weights(i)
+        xt, _ = inp.x[(m.layer, m.slot)]
+        for t in range(2):
+            x = inp.host_x(i, t)
+            want = ora.gemv(dict(fmt=fmt, w=hw[0], s=hw[1]), x) if fmt in (wl.Q4, wl.I8) else ora.gemv16(hw, x, fmt)
+            assert rel_l2(ys[i][t], want) <= TOL, (n, i, t)
+        y = torch.empty(m.M, dtype=torch.float32, device="cuda")
+        if gemv is None:
+            wsr.wsr_gemv_f16(inp.w[i], xt[1], y, m.M, K, wsr.WSR_BF16, stream())
+        else:
+            gemv(inp.w[i], inp.s[i], xt[1], y, m.M, K, stream())
+        assert np.array_equal(f32_bits(y.cpu().numpy()), f32_bits(ys[i][1])), (n, i)
