@@ -870,7 +870,13 @@ __device__ __forceinline__ void rows_q4(const DevMat& d, int64_t r0, int64_t r1,
     for (int64_t i = i_end; i < r1; ++i) q4_group<1, U>(Wq, S, x, y, nb, i, lane);
 }
 
-__device__ __forceinline__ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+/* ceil(a / b) for a >= 0, b > 0.  A 64-bit division expands to a long dependent sequence on this
+   target, so values that fit 32 bits (every range of a matrix below 4 GiB) take the 32-bit form. */
+__device__ __forceinline__ int64_t ceil_div(int64_t a, int64_t b) {
+    const uint64_t n = (uint64_t)(a + b - 1);
+    if (((n | (uint64_t)b) >> 32) == 0) return (int64_t)((uint32_t)n / (uint32_t)b);
+    return (int64_t)(n / (uint64_t)b);
+}
 
 /* Last matrix whose stream starts at or before byte lo: from the hint when it still holds, else by
    bisection over the dense offset array (8 bytes per matrix, so it stays in the scalar cache). */

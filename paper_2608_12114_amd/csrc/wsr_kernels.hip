@@ -282,17 +282,16 @@ int64_t sweep_tile(int64_t total, int64_t waves) {
     return t;
 }
 
-/* Wave w of nw takes bytes [floor(total w / nw), floor(total (w + 1) / nw)) of the stream, computed
-   without forming total * w. */
-__device__ __forceinline__ void span_bounds(int64_t total, int64_t w, unsigned nw, int64_t& lo, int64_t& hi) {
-    const int64_t q = total / nw, r = total % nw;
-    lo = q * w + (int64_t)((uint64_t)r * (uint64_t)w / nw);
-    hi = q * (w + 1) + (int64_t)((uint64_t)r * (uint64_t)(w + 1) / nw);
+/* Wave w takes bytes [w span, (w + 1) span) of the stream, cut at its end; the launcher sets span to
+   ceil(total / waves), so no division runs on the device. */
+__device__ __forceinline__ void span_bounds(int64_t total, int64_t w, int64_t span, int64_t& lo, int64_t& hi) {
+    lo = w * span;
+    hi = std::min<int64_t>(total, lo + span);
 }
 
 /* Work distribution over the weight stream [0, total) of one token:
      SCHED_TILES   tiles of `tile` bytes, claimed in order from a counter;
-     SCHED_SPANS   wave w takes [total w / nw, total (w + 1) / nw); with many more blocks than the
+     SCHED_SPANS   wave w takes [span w, span (w + 1)) (span = ceil(total / nw)); with many more blocks than the
                    chip holds at once, the hardware starts each block as an earlier one retires,
                    which balances the end of the token at no cost;
      SCHED_HYBRID  wave w first takes [span w, span (w + 1)), then the rest [span nw, total) goes out
@@ -311,7 +310,7 @@ __global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab,
     int hint = 0;
     if constexpr (SCHED == SCHED_SPANS) {
         int64_t lo, hi;
-        span_bounds(total, w, nw, lo, hi);
+        span_bounds(total, w, span, lo, hi);
         if (lo < hi) stream_range<FMT, R16, U16, RQ, UQ, QNB, T, RC, UC, RQC>(tab, cost, nmat, lo, hi, token, lane, hint);
     } else {
         int64_t base = 0;
@@ -359,13 +358,13 @@ struct TableArg {
 static_assert(sizeof(TableArg<TABLE_ARG_MAX>) + 32 <= 32000, "the by-value table must stay within the checked argument size");
 
 template <int FMT, int R16, int U16, int T, int N>
-__global__ __launch_bounds__(BLOCK) void k_sweep_arg(TableArg<N> tb, int nmat, int64_t total, int32_t token) {
+__global__ __launch_bounds__(BLOCK) void k_sweep_arg(TableArg<N> tb, int nmat, int64_t total, int64_t span,
+                                                     int32_t token) {
     const int lane = threadIdx.x & (WAVE - 1);
-    const unsigned nw = gridDim.x * WAVES_PER_BLOCK;
     const int64_t w = (int64_t)blockIdx.x * WAVES_PER_BLOCK + wave_in_block();
     int hint = 0;
     int64_t lo, hi;
-    span_bounds(total, w, nw, lo, hi);
+    span_bounds(total, w, span, lo, hi);
     if (lo < hi) stream_range<FMT, R16, U16, 8, 1, 2, T>(tb.m, tb.cost, nmat, lo, hi, token, lane, hint);
 }
 
@@ -401,12 +400,15 @@ constexpr int64_t SWEEP16_TILES_FROM = int64_t{8} << 30;
 constexpr int SPAN16_R = 2, SPAN16_U = 8;
 constexpr int64_t SWEEP_SPAN_I8[4] = {32 << 10, 32 << 10, 128 << 10, 128 << 10};   /* T = 1, 2, 4, 8 */
 
-/* Grid of a span-scheduled sweep: about `span` bytes per wave, at least one wave per SIMD. */
-static hipError_t span_grid(int64_t total, int64_t span, dim3& g) {
-    const int64_t waves = std::max<int64_t>((int64_t)cu_count() * WAVES_PER_BLOCK, (total + span - 1) / span);
+/* Grid of a span-scheduled sweep: about `target` bytes per wave, at least one wave per SIMD; *span
+   receives the bytes per wave, ceil(total / waves). */
+static hipError_t span_grid(int64_t total, int64_t target, dim3& g, int64_t* span) {
+    const int64_t waves = std::max<int64_t>((int64_t)cu_count() * WAVES_PER_BLOCK, (total + target - 1) / target);
     const int64_t blocks = (waves + WAVES_PER_BLOCK - 1) / WAVES_PER_BLOCK;
     if (blocks > INT32_MAX) return hipErrorInvalidValue;
     g = dim3((unsigned)blocks);
+    const int64_t nw = blocks * WAVES_PER_BLOCK;
+    *span = (total + nw - 1) / nw;
     return hipSuccess;
 }
 
@@ -421,21 +423,23 @@ static void fill_table_arg(TableArg<N>& tb, const DevMat* htab, int nmat) {
 /* One span-scheduled launch: the table by value when the host table is given (nmat <= TABLE_ARG_MAX),
    else from the device table. */
 template <int FMT, int T>
-static void launch_sweep_spans(dim3 g, hipStream_t s, const DevMat* tab, const int64_t* cost, const DevMat* htab,
-                               int nmat, int64_t total, int32_t token) {
+static void launch_sweep_spans(dim3 g, int64_t span, hipStream_t s, const DevMat* tab, const int64_t* cost,
+                               const DevMat* htab, int nmat, int64_t total, int32_t token) {
     constexpr int R = (FMT == FMT_F16 || FMT == FMT_BF16) ? SPAN16_R : 4;
     constexpr int U = (FMT == FMT_F16 || FMT == FMT_BF16) ? SPAN16_U : 4;
     if (htab && nmat <= TABLE_ARG_SMALL) {
         TableArg<TABLE_ARG_SMALL> tb;
         fill_table_arg(tb, htab, nmat);
-        hipLaunchKernelGGL((k_sweep_arg<FMT, R, U, T, TABLE_ARG_SMALL>), g, dim3(BLOCK), 0, s, tb, nmat, total, token);
+        hipLaunchKernelGGL((k_sweep_arg<FMT, R, U, T, TABLE_ARG_SMALL>), g, dim3(BLOCK), 0, s, tb, nmat, total, span,
+                           token);
     } else if (htab) {
         TableArg<TABLE_ARG_MAX> tb;
         fill_table_arg(tb, htab, nmat);
-        hipLaunchKernelGGL((k_sweep_arg<FMT, R, U, T, TABLE_ARG_MAX>), g, dim3(BLOCK), 0, s, tb, nmat, total, token);
+        hipLaunchKernelGGL((k_sweep_arg<FMT, R, U, T, TABLE_ARG_MAX>), g, dim3(BLOCK), 0, s, tb, nmat, total, span,
+                           token);
     } else {
         hipLaunchKernelGGL((k_sweep<FMT, SCHED_SPANS, R, U, 8, 1, 2, T>), g, dim3(BLOCK), 0, s, tab, cost, nmat,
-                           total, (int64_t)0, (int64_t)0, token, nullptr);
+                           total, span, (int64_t)0, token, nullptr);
     }
 }
 
@@ -445,13 +449,14 @@ static hipError_t launch_sweep_quant(int T, hipStream_t s, const DevMat* tab, co
                                      int nmat, int64_t total, int32_t token) {
     const int ti = T == 1 ? 0 : T == 2 ? 1 : T == 4 ? 2 : 3;
     dim3 g;
-    const hipError_t e = span_grid(total, FMT == FMT_Q4 ? SWEEP_SPAN_Q4 : SWEEP_SPAN_I8[ti], g);
+    int64_t span = 0;
+    const hipError_t e = span_grid(total, FMT == FMT_Q4 ? SWEEP_SPAN_Q4 : SWEEP_SPAN_I8[ti], g, &span);
     if (e != hipSuccess) return e;
     switch (T) {
-        case 1: launch_sweep_spans<FMT, 1>(g, s, tab, cost, htab, nmat, total, token); break;
-        case 2: launch_sweep_spans<FMT, 2>(g, s, tab, cost, htab, nmat, total, token); break;
-        case 4: launch_sweep_spans<FMT, 4>(g, s, tab, cost, htab, nmat, total, token); break;
-        case 8: launch_sweep_spans<FMT, 8>(g, s, tab, cost, htab, nmat, total, token); break;
+        case 1: launch_sweep_spans<FMT, 1>(g, span, s, tab, cost, htab, nmat, total, token); break;
+        case 2: launch_sweep_spans<FMT, 2>(g, span, s, tab, cost, htab, nmat, total, token); break;
+        case 4: launch_sweep_spans<FMT, 4>(g, span, s, tab, cost, htab, nmat, total, token); break;
+        case 8: launch_sweep_spans<FMT, 8>(g, span, s, tab, cost, htab, nmat, total, token); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -497,10 +502,11 @@ hipError_t launch_sweep(const DevMat* tab, const int64_t* cost, const DevMat* ht
     if (fmt_all == FMT_I8) return launch_sweep_quant<FMT_I8>(T, s, tab, cost, htab, nmat, total, token);
     if (sweep_spans(total, fmt_all, T)) {
         dim3 g;
-        const hipError_t e = span_grid(total, SWEEP_SPAN_16, g);
+        int64_t span = 0;
+        const hipError_t e = span_grid(total, SWEEP_SPAN_16, g, &span);
         if (e != hipSuccess) return e;
-        if (fmt_all == FMT_F16) launch_sweep_spans<FMT_F16, 1>(g, s, tab, cost, htab, nmat, total, token);
-        else launch_sweep_spans<FMT_BF16, 1>(g, s, tab, cost, htab, nmat, total, token);
+        if (fmt_all == FMT_F16) launch_sweep_spans<FMT_F16, 1>(g, span, s, tab, cost, htab, nmat, total, token);
+        else launch_sweep_spans<FMT_BF16, 1>(g, span, s, tab, cost, htab, nmat, total, token);
         return hipGetLastError();
     }
     const dim3 grid((unsigned)(cu_count() * SWEEP_BLOCKS_PER_CU_16));
