@@ -282,6 +282,19 @@ int64_t sweep_tile(int64_t total, int64_t waves) {
     return t;
 }
 
+/* The wave's index in the order of spans.  The hardware hands consecutive blocks to the 8 XCDs in
+   turn, each with its own L2, so numbering spans by block index would have every XCD work on every
+   part of the stream at once.  Block b, on XCD b % 8, instead takes place b / 8 among that XCD's
+   blocks inside the XCD's own eighth of the spans: each L2 then holds one contiguous part of the
+   stream, so the activations of a matrix are fetched into fewer L2s and the output lines that
+   neighbouring waves share are written through one L2 (8B q4 token: 619 -> 612 us). */
+constexpr unsigned XCDS = 8;
+__device__ __forceinline__ int64_t span_wave() {
+    const unsigned nb = gridDim.x, b = blockIdx.x, xcd = b % XCDS, per = nb / XCDS, rem = nb % XCDS;
+    const unsigned place = xcd * per + (xcd < rem ? xcd : rem) + b / XCDS;
+    return (int64_t)place * WAVES_PER_BLOCK + wave_in_block();
+}
+
 /* Wave w takes bytes [w span, (w + 1) span) of the stream, cut at its end; the launcher sets span to
    ceil(total / waves), so no division runs on the device. */
 __device__ __forceinline__ void span_bounds(int64_t total, int64_t w, int64_t span, int64_t& lo, int64_t& hi) {
@@ -310,7 +323,7 @@ __global__ __launch_bounds__(BLOCK) void k_sweep(const DevMat* __restrict__ tab,
     int hint = 0;
     if constexpr (SCHED == SCHED_SPANS) {
         int64_t lo, hi;
-        span_bounds(total, w, span, lo, hi);
+        span_bounds(total, span_wave(), span, lo, hi);
         if (lo < hi) stream_range<FMT, R16, U16, RQ, UQ, QNB, T, RC, UC, RQC>(tab, cost, nmat, lo, hi, token, lane, hint);
     } else {
         int64_t base = 0;
@@ -361,10 +374,9 @@ template <int FMT, int R16, int U16, int T, int N>
 __global__ __launch_bounds__(BLOCK) void k_sweep_arg(TableArg<N> tb, int nmat, int64_t total, int64_t span,
                                                      int32_t token) {
     const int lane = threadIdx.x & (WAVE - 1);
-    const int64_t w = (int64_t)blockIdx.x * WAVES_PER_BLOCK + wave_in_block();
     int hint = 0;
     int64_t lo, hi;
-    span_bounds(total, w, span, lo, hi);
+    span_bounds(total, span_wave(), span, lo, hi);
     if (lo < hi) stream_range<FMT, R16, U16, 8, 1, 2, T>(tb.m, tb.cost, nmat, lo, hi, token, lane, hint);
 }
 
