@@ -78,7 +78,9 @@ def parse():
     p.add_argument("--workload", default="llama70b_bf16", choices=["llama70b_bf16", "llama8b_q4"])
     p.add_argument("--rows", default="probe,gemv_f16,llama8b_q4,protocol,endpoints,ordering,size_sweep,bus",
                    help="comma list of extra rows ('' for none)")
-    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle baselines of every row")
+    p.add_argument("--no-mapped", action="store_true",
+                   help="skip the host-mapped arms of the probe and the size sweep (resident-only profiles)")
     p.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle time of the sample")
     p.add_argument("--passes", type=int, default=4, help="extra timed passes for the spread")
     p.add_argument("--processes", type=int, default=0,
@@ -266,17 +268,43 @@ def oracle_gemv(ora, fmt, hw, x, threads=1):
     return ora.gemv16(hw, x, fmt, threads=threads)
 
 
+def oracle_threads():
+    """Host threads for the oracle's all-core mode: every core this process may run on, capped by
+    OMP_NUM_THREADS where that is set lower (a GPU machine grants the process a share of its cores).
+    Returns (threads used, cores available, the cap's source or None)."""
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count() or 1
+    cap = os.environ.get("OMP_NUM_THREADS", "")
+    if cap.isdigit() and 0 < int(cap) < avail:
+        return int(cap), avail, f"OMP_NUM_THREADS={cap}"
+    return avail, avail, None
+
+
+def core_fields(threads, avail, cap):
+    return {"cores": threads, "cores_available": avail, "thread_cap": cap}
+
+
+def time_until(fn, seconds, max_calls=1 << 30):
+    """Calls fn() until `seconds` have passed (at least once); returns (calls, seconds spent)."""
+    t0 = time.perf_counter()
+    n = 0
+    while n < max_calls:
+        fn()
+        n += 1
+        if time.perf_counter() - t0 >= seconds:
+            break
+    return n, time.perf_counter() - t0
+
+
 def cpu_baseline(inp, bpt, seconds):
     """The oracle as it stands, all host cores, on the first matrices of token 0 until about
     `seconds` of oracle time; scaled to the whole token."""
     import oracle
     from synth import workloads as wl
     ora = oracle.get()
-    try:
-        threads = len(os.sched_getaffinity(0))
-    except AttributeError:
-        threads = os.cpu_count() or 1
-    threads = min(threads, 16)
+    threads, avail, cap = oracle_threads()
     spent, nbytes, names = 0.0, 0, []
     for i, m in enumerate(inp.mats):
         hw = inp.host_weights(i)
@@ -299,8 +327,9 @@ def cpu_baseline(inp, bpt, seconds):
     m0 = inp.mats[0]
     rate1 = wl.matrix_bytes(m0.M, m0.K, inp.fmts[0]) / one
     log(f"cpu oracle, one thread: L{m0.layer}.{m0.name} in {one:.2f} s -> {rate1 / 1e9:.2f} GB/s")
-    return {"value": rate / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
+    return {"value": rate / 1e9, "unit": "GB/s", **core_fields(threads, avail, cap), "kind": "oracle",
             "single_thread": {"value": rate1 / 1e9, "unit": "GB/s", "cores": 1, "seconds": one,
+                              "tokens_per_s": rate1 / bpt,
                               "sample": f"token 0, L{m0.layer}.{m0.name} ({m0.M} x {m0.K})"},
             "tokens_per_s": rate / bpt, "seconds": spent,
             "sample": f"token 0, first {len(names)} matrices in sweep order ({names[0]} .. {names[-1]}), "
@@ -310,14 +339,43 @@ def cpu_baseline(inp, bpt, seconds):
 # --------------------------------------------------------------------------------------------------
 # extra rows
 
-def row_probe(stream, wsr):
+def probe_cpu_baseline(host):
+    """The oracle's probe sum on the host copy of the first buffer: one thread over the whole
+    buffer, and all cores over contiguous parts of it (one ctypes call per thread; ctypes releases
+    the GIL), the parts' sums added in order.  On the 2^-23 grid every sum is exact, so both modes
+    must give the same value."""
+    import oracle
+    from concurrent.futures import ThreadPoolExecutor
+    ora = oracle.get()
+    threads, avail, cap = oracle_threads()
+    nb = host.nbytes
+    t0 = time.perf_counter()
+    s1 = ora.probe_sum(host)
+    one = time.perf_counter() - t0
+    parts = np.array_split(host, threads)
+    with ThreadPoolExecutor(threads) as ex:
+        t0 = time.perf_counter()
+        sums = list(ex.map(ora.probe_sum, parts))
+        allc = time.perf_counter() - t0
+    total = 0.0
+    for v in sums:
+        total += v
+    log(f"cpu oracle, probe: one thread {nb / one / 1e9:.2f} GB/s, {threads} threads {nb / allc / 1e9:.2f} GB/s")
+    return {"value": nb / allc / 1e9, "unit": "GB/s", **core_fields(threads, avail, cap), "kind": "oracle",
+            "seconds": allc, "sums_equal": bool(total == s1),
+            "single_thread": {"value": nb / one / 1e9, "unit": "GB/s", "cores": 1, "seconds": one},
+            "sample": "the whole 1 GiB buffer (2^28 fp32 values), both modes"}
+
+
+def row_probe(stream, wsr, mapped=True, want_cpu=True):
     import torch
     import synth
     from synth import device as dv
     from synth import workloads as wl
     n = wl.PROBE_N
     nb = n * 4
-    bufs = [dv.to_device(synth.grid_f32(n, seed=0, stream=1 + k)) for k in range(4)]
+    first = synth.grid_f32(n, seed=0, stream=1)
+    bufs = [dv.to_device(first)] + [dv.to_device(synth.grid_f32(n, seed=0, stream=1 + k)) for k in range(1, 4)]
     out = torch.zeros(1, dtype=torch.float64, device="cuda")
     ws = torch.zeros(wsr.wsr_probe_workspace_bytes(n), dtype=torch.uint8, device="cuda")
     call = lambda b: wsr.wsr_probe_read(b, n, out, ws, ws.numel(), stream)
@@ -331,9 +389,15 @@ def row_probe(stream, wsr):
         k[0] += 1
     rotated = median_of(rot, 20, 5, stream) / 20
     res = {"bytes": nb, "resident_GBps": nb / rotated / 1e9, "resident_same_buffer_GBps": nb / same / 1e9,
-           "resident_us": rotated * 1e6}
+           "resident_us": rotated * 1e6, "hbm_frac": nb / rotated / HBM_PEAK}
     del bufs
     torch.cuda.empty_cache()
+    if want_cpu:
+        res["cpu_baseline"] = probe_cpu_baseline(first)
+    del first
+    if not mapped:
+        log(f"probe: resident {res['resident_GBps']:.1f} GB/s (same buffer {res['resident_same_buffer_GBps']:.1f})")
+        return res
     # host-mapped: the same kernel over pinned host pages read in place across PCIe
     host = torch.empty(nb, dtype=torch.uint8, pin_memory=True)
     synth.grid_f32(n, seed=0, stream=1, out=host.numpy().view(np.float32))
@@ -349,15 +413,41 @@ def row_probe(stream, wsr):
     return res
 
 
-def row_gemv_f16(stream, wsr):
+def gemv_cpu_baseline(mats, x, fmt, seconds, what):
+    """The oracle's 16-bit GEMV over host matrices (visited in turn) for about `seconds` in each
+    mode: one thread, then all cores (OpenMP over rows)."""
+    import oracle
+    ora = oracle.get()
+    threads, avail, cap = oracle_threads()
+    out = {}
+    for mode, th in (("single_thread", 1), ("all", threads)):
+        k = [0]
+
+        def one():
+            ora.gemv16(mats[k[0] % len(mats)], x, fmt, threads=th)
+            k[0] += 1
+        calls, sec = time_until(one, seconds)
+        nbytes = sum(mats[i % len(mats)].nbytes for i in range(calls))
+        out[mode] = {"value": nbytes / sec / 1e9, "unit": "GB/s", "calls": calls, "seconds": sec,
+                     "gemv_per_s": calls / sec}
+    log(f"cpu oracle, {what}: one thread {out['single_thread']['value']:.2f} GB/s, "
+        f"{threads} threads {out['all']['value']:.2f} GB/s")
+    return {"value": out["all"]["value"], "unit": "GB/s", **core_fields(threads, avail, cap), "kind": "oracle",
+            "seconds": out["all"]["seconds"], "gemv_per_s": out["all"]["gemv_per_s"],
+            "single_thread": dict(out["single_thread"], cores=1),
+            "sample": f"{what}, about {seconds:g} s per mode"}
+
+
+def row_gemv_f16(stream, wsr, want_cpu=True):
     import torch
     import synth
     from synth import device as dv
     from synth import workloads as wl
     cfg = wl.GemvConfig()
-    Ws = [dv.to_device(synth.normal16((cfg.M, cfg.K), wl.W_SIGMA, "f16", seed=0, stream=1 + b))
-          for b in range(cfg.rotate)]
-    x = dv.to_device(synth.normal16(cfg.K, wl.X_SIGMA, "f16", seed=0, stream=1000))
+    host_W = [synth.normal16((cfg.M, cfg.K), wl.W_SIGMA, "f16", seed=0, stream=1 + b) for b in range(cfg.rotate)]
+    host_x = synth.normal16(cfg.K, wl.X_SIGMA, "f16", seed=0, stream=1000)
+    Ws = [dv.to_device(W) for W in host_W]
+    x = dv.to_device(host_x)
     y = torch.empty((cfg.rotate, cfg.M), dtype=torch.float32, device="cuda")
     bytes_one = cfg.M * cfg.K * 2
 
@@ -377,18 +467,24 @@ def row_gemv_f16(stream, wsr):
     tw = median_of(lambda: wsr.wsr_gemv_f16(Ws[0], x, y[0], cfg.M, cfg.K, wsr.WSR_F16, stream), cfg.rotate, 15,
                    stream) / cfg.rotate
     res = {"bytes_per_gemv": bytes_one, "us_per_gemv": per * 1e6, "GBps_per_dispatch": bytes_one / per / 1e9,
+           "hbm_frac_per_dispatch": bytes_one / per / HBM_PEAK,
            "one_launch_32_matrices_GBps": bytes_one * cfg.rotate / tf / 1e9,
+           "one_launch_32_matrices_hbm_frac": bytes_one * cfg.rotate / tf / HBM_PEAK,
+           "one_launch_us": tf * 1e6,
            "single_buffer_cache_warm": {"us_per_gemv": tw * 1e6, "GBps": bytes_one / tw / 1e9,
                                         "note": "one 32 MiB matrix repeated: served from the Infinity Cache, not HBM"}}
     log(f"gemv_f16 4096x4096: {per * 1e6:.2f} us/GEMV ({res['GBps_per_dispatch']:.1f} GB/s over 32 dispatches); "
         f"one launch over all 32: {res['one_launch_32_matrices_GBps']:.1f} GB/s; one buffer repeated "
         f"(cache-warm): {tw * 1e6:.2f} us/GEMV")
+    if want_cpu:
+        res["cpu_baseline"] = gemv_cpu_baseline(host_W, host_x, "f16", 2.0,
+                                                f"the 32 rotated {cfg.M} x {cfg.K} fp16 matrices in turn")
     del Ws
     torch.cuda.empty_cache()
     return res
 
 
-def row_protocol(stream, wsr, warmup_passes=12, passes=31, tokens=16):
+def row_protocol(stream, wsr, warmup_passes=12, passes=31, tokens=16, want_cpu=True):
     """The matched protocol of Sec. 3.1: a pass is one single-token int8 GEMV (fp16 row scales) over
     each of 12 distinct 12288 x 7168 matrices, bracketed by one synchronisation; the first 12
     passes are discarded and the median pass is reported, counting weight bytes once.  Measured as
@@ -453,6 +549,8 @@ def row_protocol(stream, wsr, warmup_passes=12, passes=31, tokens=16):
     log(f"protocol: parity on sampled rows: worst rel-L2 {res['parity']['worst_rel_l2']:.2e}")
     res["batched"] = batch_sweep("protocol", inp, specs, ws, tokens, nbytes, stream, wsr, (1, 2, 4, 8))
     res["batched_matrix_cores"] = mma_sweep("protocol", inp, specs, ws, tokens, nbytes, stream, wsr)
+    if want_cpu:
+        res["cpu_baseline"] = cpu_baseline(inp, nbytes, 3.0)
     del specs, ws, inp
     torch.cuda.empty_cache()
     return res
@@ -650,49 +748,75 @@ def row_ordering(stream, wsr, depths=(2, 8, 32), steps=20, reps=7, seed=0, workl
     return res
 
 
-def row_size_sweep(stream, wsr):
+def row_size_sweep(stream, wsr, mapped=True, want_cpu=True):
+    """The bf16 matrix-size sweep (Sec. 3.4) in both readings of its shapes: reduction length 4096
+    with N output rows, and 4096 output rows with reduction length N, for the 12 sizes of N.  Both
+    readings stream the same bytes per matrix, so they share the weight buffers: resident (rotated
+    over at least 1 GiB of distinct buffers, and one buffer repeated) and host-mapped (one pinned
+    buffer read in place)."""
     import torch
     import synth
     from synth import device as dv
     from synth import workloads as wl
-    K = wl.SWEEP_K
-    x = dv.to_device(synth.normal16(K, wl.X_SIGMA, "bf16", seed=0, stream=2))
-    out = []
+    K0 = wl.SWEEP_K
     maxN = max(wl.SWEEP_N)
-    host = torch.empty(maxN * K * 2, dtype=torch.uint8, pin_memory=True)
-    synth.normal16(maxN * K, wl.W_SIGMA, "bf16", seed=0, stream=1, out=host.numpy().view(np.uint16))
-    hdev, granted = wsr.wsr_register_host(host, host.numel(), 0)
+    x_rows_host = synth.normal16(K0, wl.X_SIGMA, "bf16", seed=0, stream=2)
+    x_rows = dv.to_device(x_rows_host)
+    x_cols_host = synth.normal16(maxN, wl.X_SIGMA, "bf16", seed=0, stream=3)
+    x_cols = dv.to_device(x_cols_host)
+    host = torch.empty(maxN * K0 * 2, dtype=torch.uint8, pin_memory=True)
+    synth.normal16(maxN * K0, wl.W_SIGMA, "bf16", seed=0, stream=1, out=host.numpy().view(np.uint16))
+    hdev = None
+    if mapped:
+        hdev, granted = wsr.wsr_register_host(host, host.numel(), 0)
+    readings = {"rows": [], "cols": []}    # rows: M = N, K = 4096; cols: M = 4096, K = N
     try:
         for N in wl.SWEEP_N:
-            nbytes = N * K * 2
+            nbytes = N * K0 * 2
             rot = max(1, -(-(1 << 30) // nbytes))   # distinct buffers per pass: at least 1 GiB
-            Ws = [torch.empty(N * K, dtype=torch.int16, device="cuda") for _ in range(rot)]
+            Ws = [torch.empty(N * K0, dtype=torch.int16, device="cuda") for _ in range(rot)]
             for W in Ws:
                 W.view(torch.uint8).copy_(host[:nbytes], non_blocking=True)
-            y = torch.empty(N, dtype=torch.float32, device="cuda")
-            k = [0]
+            for name, M, K, x in (("rows", N, K0, x_rows), ("cols", K0, N, x_cols)):
+                y = torch.empty(M, dtype=torch.float32, device="cuda")
+                k = [0]
 
-            def res_call():
-                wsr.wsr_gemv_f16(Ws[k[0] % rot], x, y, N, K, wsr.WSR_BF16, stream)
-                k[0] += 1
-            res_call()
-            reps = max(rot, 8)
-            tr = median_of(res_call, reps, 5, stream) / reps
-            ts = median_of(lambda: wsr.wsr_gemv_f16(Ws[0], x, y, N, K, wsr.WSR_BF16, stream), 8, 5, stream) / 8
-            tm = median_of(lambda: wsr.wsr_gemv_f16(hdev, x, y, N, K, wsr.WSR_BF16, stream), 1, 3, stream)
-            out.append({"N": N, "bytes": nbytes, "resident_GBps": nbytes / tr / 1e9,
-                        "resident_same_buffer_GBps": nbytes / ts / 1e9, "mapped_GBps": nbytes / tm / 1e9,
-                        "resident_us": tr * 1e6})
-            log(f"size sweep N={N:6d} ({nbytes / 2**20:7.1f} MiB): resident {nbytes / tr / 1e9:7.1f} GB/s, "
-                f"same-buffer {nbytes / ts / 1e9:7.1f}, host-mapped {nbytes / tm / 1e9:6.1f}")
+                def res_call():
+                    wsr.wsr_gemv_f16(Ws[k[0] % rot], x, y, M, K, wsr.WSR_BF16, stream)
+                    k[0] += 1
+                res_call()
+                reps = max(rot, 8)
+                tr = median_of(res_call, reps, 5, stream) / reps
+                ts = median_of(lambda: wsr.wsr_gemv_f16(Ws[0], x, y, M, K, wsr.WSR_BF16, stream), 8, 5, stream) / 8
+                pt = {"N": N, "M": M, "K": K, "bytes": nbytes, "resident_GBps": nbytes / tr / 1e9,
+                      "resident_same_buffer_GBps": nbytes / ts / 1e9, "resident_us": tr * 1e6,
+                      "hbm_frac": nbytes / tr / HBM_PEAK}
+                if mapped:
+                    tm = median_of(lambda: wsr.wsr_gemv_f16(hdev, x, y, M, K, wsr.WSR_BF16, stream), 1, 3, stream)
+                    pt["mapped_GBps"] = nbytes / tm / 1e9
+                readings[name].append(pt)
+                log(f"size sweep {name} M={M:6d} K={K:6d} ({nbytes / 2**20:7.1f} MiB): resident {nbytes / tr / 1e9:7.1f} GB/s, "
+                    f"same-buffer {nbytes / ts / 1e9:7.1f}" + (f", host-mapped {pt['mapped_GBps']:6.1f}" if mapped else ""))
             del Ws
             torch.cuda.empty_cache()
     finally:
-        wsr.wsr_unregister_host(host)
-    return {"points": out, "crossovers": size_crossovers(out)}
+        if mapped:
+            wsr.wsr_unregister_host(host)
+    out = {"points": readings["rows"], "crossovers": size_crossovers(readings["rows"], "rows"),
+           "transposed": {"points": readings["cols"], "crossovers": size_crossovers(readings["cols"], "cols"),
+                          "shape": "M = 4096 output rows, K = N"},
+           "shape": "M = N output rows, K = 4096"}
+    if want_cpu:
+        W = host.numpy().view(np.uint16)
+        out["cpu_baseline"] = gemv_cpu_baseline([W.reshape(maxN, K0)], x_rows_host, "bf16", 2.0,
+                                                f"the largest matrix, {maxN} x {K0} bf16 (1.15 GB)")
+        out["transposed"]["cpu_baseline"] = gemv_cpu_baseline([W.reshape(K0, maxN)], x_cols_host, "bf16", 2.0,
+                                                              f"the largest matrix, {K0} x {maxN} bf16 (1.15 GB)")
+    del host
+    return out
 
 
-def size_crossovers(pts):
+def size_crossovers(pts, name="rows"):
     """The size sweep's three crossovers (Sec. 3.4's matrix-size sweep): (i) dispatch, the smallest
     size whose resident rate reaches half the plateau; (ii) MALL, the smallest size from which the
     single-buffer repeat rate stays within 2 % of the rotated rate (below it the repeated buffer
@@ -706,7 +830,7 @@ def size_crossovers(pts):
             mall = pts[i]
             break
     best = max(pts, key=lambda p: p["resident_same_buffer_GBps"] / p["resident_GBps"])
-    mapped = next((p for p in pts if p["mapped_GBps"] >= p["resident_GBps"]), None)
+    mapped = next((p for p in pts if p.get("mapped_GBps", 0.0) >= p["resident_GBps"]), None)
     out = {"resident_plateau_GBps": plateau,
            "dispatch": {"bytes": disp["bytes"], "N": disp["N"], "resident_GBps": disp["resident_GBps"],
                         "paper_context": "about 23 MB on the paper's machine (Sec. 3.4); context, not a target"},
@@ -714,9 +838,11 @@ def size_crossovers(pts):
            "largest_repeat_gain": {"bytes": best["bytes"],
                                    "same_buffer_over_rotated": best["resident_same_buffer_GBps"] / best["resident_GBps"]},
            "mapped_equals_resident": None if mapped is None else {"bytes": mapped["bytes"], "N": mapped["N"]}}
+    if not any("mapped_GBps" in p for p in pts):
+        out["mapped_equals_resident"] = "not measured"
     mall_txt = "none" if mall is None else f"{mall['bytes'] / 1e6:.1f} MB"
     mapped_txt = "never" if mapped is None else f"{mapped['bytes'] / 1e6:.1f} MB"
-    log(f"size sweep: plateau {plateau:.0f} GB/s; dispatch crossover {disp['bytes'] / 1e6:.1f} MB; "
+    log(f"size sweep {name}: plateau {plateau:.0f} GB/s; dispatch crossover {disp['bytes'] / 1e6:.1f} MB; "
         f"MALL crossover {mall_txt}; mapped = resident: {mapped_txt}")
     return out
 
@@ -796,18 +922,19 @@ def main():
     head = run_sweep(args.workload, args.steps, args.warmup, stream, wsr, not args.no_cpu_baseline,
                      args.cpu_seconds, args.passes)
     rows = {}
+    cpu = not args.no_cpu_baseline
     for r in [r for r in args.rows.split(",") if r]:
         if r == "probe":
-            rows[r] = row_probe(stream, wsr)
+            rows[r] = row_probe(stream, wsr, mapped=not args.no_mapped, want_cpu=cpu)
         elif r == "gemv_f16":
-            rows[r] = row_gemv_f16(stream, wsr)
+            rows[r] = row_gemv_f16(stream, wsr, want_cpu=cpu)
         elif r == "llama8b_q4":
             if args.workload != "llama8b_q4":
-                rows[r] = run_sweep("llama8b_q4", 64, 4, stream, wsr, False, 0, warm_seconds=0.5)
+                rows[r] = run_sweep("llama8b_q4", 64, 4, stream, wsr, cpu, 3.0, warm_seconds=0.5)
         elif r == "size_sweep":
-            rows[r] = row_size_sweep(stream, wsr)
+            rows[r] = row_size_sweep(stream, wsr, mapped=not args.no_mapped, want_cpu=cpu)
         elif r == "protocol":
-            rows[r] = row_protocol(stream, wsr)
+            rows[r] = row_protocol(stream, wsr, want_cpu=cpu)
         elif r == "endpoints":
             rows[r] = row_endpoints(stream, wsr)
         elif r == "ordering":

@@ -62,3 +62,33 @@ def test_more_than_one_gpu_exits_with_a_message():
                        capture_output=True, text=True, timeout=120, cwd=ROOT)
     assert r.returncode != 0
     assert "one GPU" in (r.stdout + r.stderr) or "1 GPU" in (r.stdout + r.stderr) or "single" in (r.stdout + r.stderr)
+
+
+def test_oracle_threads_records_the_cap(monkeypatch):
+    avail = len(os.sched_getaffinity(0))
+    monkeypatch.delenv("OMP_NUM_THREADS", raising=False)
+    assert bench.oracle_threads() == (avail, avail, None)
+    if avail > 1:
+        monkeypatch.setenv("OMP_NUM_THREADS", "1")
+        assert bench.oracle_threads() == (1, avail, "OMP_NUM_THREADS=1")
+    monkeypatch.setenv("OMP_NUM_THREADS", str(avail + 7))      # a cap above the cores is no cap
+    assert bench.oracle_threads() == (avail, avail, None)
+
+
+def test_size_crossovers_without_mapped_arm():
+    pts = [{"N": n, "bytes": n * 8192, "resident_GBps": r, "resident_same_buffer_GBps": r}
+           for n, r in ((256, 500), (512, 4000), (1024, 7000))]
+    c = bench.size_crossovers(pts)
+    assert c["dispatch"]["N"] == 512 and c["mapped_equals_resident"] == "not measured"
+
+
+def test_probe_and_gemv_oracle_baselines_on_small_inputs():
+    import synth
+    buf = synth.grid_f32((1 << 16) + 3, seed=0, stream=1)
+    r = bench.probe_cpu_baseline(buf)
+    assert r["kind"] == "oracle" and r["sums_equal"] and r["value"] > 0 and r["single_thread"]["cores"] == 1
+    assert r["cores"] >= 1 and r["cores_available"] >= r["cores"]
+    W = [synth.normal16((64, 256), 0.02, "f16", seed=0, stream=5 + i) for i in range(3)]
+    x = synth.normal16(256, 1.0, "f16", seed=0, stream=9)
+    g = bench.gemv_cpu_baseline(W, x, "f16", 0.05, "three small matrices")
+    assert g["value"] > 0 and g["single_thread"]["calls"] >= 1 and g["sample"].startswith("three small")
