@@ -35,7 +35,7 @@ def dec(codes, fmt):
 
 
 SHAPES16 = [(1, 8), (3, 24), (37, 520), (64, 4104), (257, 4096), (4096, 4096), (1000, 14336),
-            (9000, 1024), (2, 28672)]
+            (9000, 1024), (2, 28672), (4099, 65536)]   # the last: rows of 128 KiB, four per wave
 
 
 @pytest.mark.parametrize("fmt", ["f16", "bf16"])
@@ -90,6 +90,19 @@ def test_gemv_bf16_size_sweep_config(N):
     x = synth.normal16(K, wl.X_SIGMA, "bf16", seed=0, stream=2)
     y = gemv16(W, x, "bf16", N, K)
     rows = sample_rows(N, 256)
+    yo = oracle.get().gemv16(W[rows], x, "bf16", threads=8)
+    assert rel_l2(y[rows], yo) <= TOL
+
+
+@pytest.mark.parametrize("N", wl.SWEEP_N)
+def test_gemv_bf16_size_sweep_transposed(N):
+    """The size sweep's other reading: 4096 output rows, reduction length N (up to 140,800: rows of
+    275 KiB), the same bytes per matrix as the shapes above."""
+    M = wl.SWEEP_K
+    W = synth.normal16((M, N), wl.W_SIGMA, "bf16", seed=0, stream=1)
+    x = synth.normal16(N, wl.X_SIGMA, "bf16", seed=0, stream=3)
+    y = gemv16(W, x, "bf16", M, N)
+    rows = sample_rows(M, 256)
     yo = oracle.get().gemv16(W[rows], x, "bf16", threads=8)
     assert rel_l2(y[rows], yo) <= TOL
 
