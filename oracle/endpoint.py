@@ -1,27 +1,22 @@
-"""Oracle of Alg. 2, endpoint selection at deployment (paper Sec. 8.1) - TEST INFRASTRUCTURE ONLY.
+"""Oracle of endpoint selection at deployment (Alg. 2, paper Sec. 8.1) - TEST INFRASTRUCTURE ONLY.
 
 Only `tests/` and `bench.py` may import this module; the library's own selection is C code that
 shares nothing with it.
 
-The procedure, in the paper's order, for a working set W and three endpoints (map: the kernel
-reads the file pages in place; resident: one copy into device memory serves every pass; copy: the
-bytes are staged into device memory for each use):
-  1. W is mapped and every page faulted in.
-  2. A mapped set that is still not resident ends the procedure with a storage-bound verdict.
-  3. B_map is measured over the whole mapped set.
-  4. A resident arm is built that holds all of W.
-  5. The resident endpoint leaves the race if that allocation failed or if one pass of every arm
-     pushed the mapping out of memory.
-  6. B_dev and B_copy are measured with the same kernel over the same set.
-  7. Endpoints that break an import or capacity limit leave the race.
-  8. The survivors are ordered by path time W / B; map wins whenever it is within the band theta
-     (5 %) of the best, since it keeps a single evictable copy of the bytes.
-  9. Otherwise the fastest survivor is the answer.
-Steps 1, 3, 4 and 6 are measurements and arrive here as inputs.
+The rule, for a working set of W bytes and three endpoints (map: the kernel reads the file pages in
+place; resident: one copy in device memory serves every pass; copy: the bytes are staged into
+device memory for each use), given their measured rates and two residency facts:
+  - a mapped set that is not resident after prefaulting lies outside the regime the selection
+    covers, and the answer is "storage-bound";
+  - an endpoint leaves the race when its rate is absent, when an import or capacity limit excludes
+    it, and (resident only) when its allocation failed or one pass of every arm evicted the mapping;
+  - each remaining endpoint costs its path time W / B;
+  - map wins whenever its path time lies within the tie band theta of the fastest, since it keeps a
+    single evictable copy of the bytes; otherwise the fastest endpoint wins.
+The rates and residency facts are measurements and arrive here as inputs.
 
-Reading of step 8 (the paper gives no formula): "within theta" compares map's time with the
-fastest survivor's, relative to the fastest: t_map - t_min <= theta * t_min.  Rates that are absent
-(None or <= 0) count as endpoints that were not measured and are dropped with those of step 7.
+The paper gives no formula for the band.  The reading used here compares map's time with the
+fastest remaining endpoint's, relative to the fastest: t_map - t_min <= theta * t_min.
 """
 from __future__ import annotations
 
@@ -39,24 +34,20 @@ def select_endpoint(w_bytes: float, b_map, b_resident, b_copy, theta: float = 0.
                     mapped_resident: bool = True, resident_ok: bool = True, excluded=()):
     """Returns (choice, by_tie): choice in ENDPOINTS, "storage-bound" or "none"; by_tie is True
     when map was chosen by the band rather than as the outright fastest."""
-    # step 2
+    # a mapped set that is not resident: outside the regime
     if not mapped_resident:
         return "storage-bound", False
     times = {"map": path_time_ms(w_bytes, b_map), "resident": path_time_ms(w_bytes, b_resident),
              "copy": path_time_ms(w_bytes, b_copy)}
-    # step 5
-    if not resident_ok:
+    if not resident_ok:                           # allocation failed or the mapping was evicted
         times["resident"] = None
-    # step 7 (and endpoints without a measured rate)
-    for e in excluded:
+    for e in excluded:                            # import or capacity limits
         times[e] = None
     survivors = {e: t for e, t in times.items() if t is not None}
     if not survivors:
         return "none", False
-    # step 8
     fastest = min(survivors, key=lambda e: (survivors[e], ENDPOINTS.index(e)))
     t_min = survivors[fastest]
-    if "map" in survivors and survivors["map"] - t_min <= theta * t_min:
+    if "map" in survivors and survivors["map"] - t_min <= theta * t_min:   # the tie band
         return "map", fastest != "map"
-    # step 9
     return fastest, False

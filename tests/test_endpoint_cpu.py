@@ -23,7 +23,7 @@ def rate(t_ms):
 
 
 def table_case(row, theta, mod=ep):
-    # a resident time of null is the GH200 set that exceeds device memory: a capacity limit (step 7)
+    # a resident time of null is the GH200 set that exceeds device memory: a capacity limit
     excluded = ("resident",) if row["resident_ms"] is None else ()
     return mod.select_endpoint(W, rate(row["map_ms"]), rate(row["resident_ms"]), rate(row["copy_ms"]),
                                theta=theta, excluded=excluded)
