@@ -39,10 +39,13 @@ __global__ __launch_bounds__(WAVE) void k_sweep_mma(const DevMat* __restrict__ t
     const int64_t hi = base + q * (k + 1) + (int64_t)((uint64_t)r * (uint64_t)(k + 1) / nw);
     int hint = 0;
     if (lo >= hi) return;
+    /* the q4 activation ring: two units of 8 slabs of 64 16-byte chunks (16 KiB) */
+    __shared__ u32x4 xlds[2 * MmaStep<FMT_Q4>::SLABS * WAVE];
     if (main)
-        stream_range_mma<FMT, MMA_TILES>(tab, cost, nmat, lo, hi, 0, 16 * MMA_TILES, token0, ntok, lane, hint);
+        stream_range_mma<FMT, MMA_TILES>(tab, cost, nmat, lo, hi, 0, 16 * MMA_TILES, token0, ntok, lane, hint, xlds);
     else
-        stream_range_mma<FMT, MMA_TAIL_TILES>(tab, cost, nmat, lo, hi, tail, 16 * MMA_TILES, token0, ntok, lane, hint);
+        stream_range_mma<FMT, MMA_TAIL_TILES>(tab, cost, nmat, lo, hi, tail, 16 * MMA_TILES, token0, ntok, lane, hint,
+                                              xlds);
 }
 
 int64_t mma_group_rows() { return 16 * MMA_TILES; }
