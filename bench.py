@@ -47,7 +47,9 @@ def log(*a):
 
 KERNEL_SOURCES = ("paper_2608_12114_amd/csrc/wsr_device.h", "paper_2608_12114_amd/csrc/wsr_kernels.hip",
                   "paper_2608_12114_amd/csrc/wsr_internal.h", "paper_2608_12114_amd/build.py")
-PROFILE_OF = {"llama70b_bf16": "k_sweep_bf16_llama70b", "llama8b_q4": "k_sweep_q4_llama8b"}
+PROFILE_OF = {"llama70b_bf16": "k_sweep_bf16_llama70b", "llama8b_q4": "k_sweep_q4_llama8b",
+              "probe": "k_probe_1gib", "gemv_f16": "k_gemv16_f16_4096x4096",
+              "gemv_f16_one_launch": "k_sweep_f16_32x4096x4096", "protocol": "k_sweep_i8_protocol"}
 
 
 def kernel_sources_sha256() -> str:
@@ -58,16 +60,29 @@ def kernel_sources_sha256() -> str:
     return h.hexdigest()
 
 
-def profiled_traffic(workload):
+def profiled_traffic(key):
     """HBM bytes per launch from the committed rocprofv3 counter summary (FETCH_SIZE + WRITE_SIZE,
     each scaled by the copy-kernel calibration), or None when the kernel sources changed since."""
-    path = os.path.join(ROOT, "profiles", PROFILE_OF[workload] + ".json")
+    path = os.path.join(ROOT, "profiles", PROFILE_OF[key] + ".json")
     if not os.path.exists(path):
         return None, "no profile"
     rec = json.load(open(path))
     if rec.get("kernel_source_sha256") != kernel_sources_sha256():
         return None, "kernel changed since the counters were taken"
     return rec.get("traffic_bytes_per_launch"), os.path.relpath(path, ROOT)
+
+
+def row_roofline(gbps, key, bytes_per_launch):
+    """The roofline object of a row: HBM-bound, the row's own rate against the 8 TB/s peak, and the
+    HBM bytes per launch its profile measured (null once the kernels changed since)."""
+    traffic, src = profiled_traffic(key)
+    kernel = None
+    path = os.path.join(ROOT, "profiles", PROFILE_OF[key] + ".json")
+    if os.path.exists(path):
+        kernel = json.load(open(path)).get("kernel")
+    return {"bound": "hbm", "achieved": round(gbps, 2), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+            "frac": round(gbps * 1e9 / HBM_PEAK, 4), "traffic": traffic, "traffic_source": src, "kernel": kernel,
+            "bytes_per_launch": bytes_per_launch}
 
 
 def parse():
@@ -173,7 +188,8 @@ def run_sweep(name, steps, warmup, stream, wsr, want_cpu, cpu_seconds, passes=4,
     out = {"workload": name, "bytes_per_token": bpt, "footprint_bytes": wl.footprint_bytes(shape, fmt),
            "tokens_timed": steps, "warmup_tokens": warmup, "ms_per_token": per_tok * 1e3,
            "GBps": gbps, "hbm_frac": gbps * 1e9 / HBM_PEAK, "tokens_per_s": 1 / per_tok,
-           "launches_per_token": 1, "parity": parity, "passes": spread(pass_ms)}
+           "launches_per_token": 1, "parity": parity, "passes": spread(pass_ms),
+           "roofline": row_roofline(gbps, name, bpt)}
     if batched is not None:
         out["batched"] = batched
     out["batched_matrix_cores"] = mma_sweep(name, inp, specs, ws, steps, bpt, stream, wsr)
@@ -392,6 +408,7 @@ def row_probe(stream, wsr, mapped=True, want_cpu=True):
            "resident_us": rotated * 1e6, "hbm_frac": nb / rotated / HBM_PEAK}
     del bufs
     torch.cuda.empty_cache()
+    res["roofline"] = row_roofline(res["resident_GBps"], "probe", nb)
     if want_cpu:
         res["cpu_baseline"] = probe_cpu_baseline(first)
     del first
@@ -476,6 +493,9 @@ def row_gemv_f16(stream, wsr, want_cpu=True):
     log(f"gemv_f16 4096x4096: {per * 1e6:.2f} us/GEMV ({res['GBps_per_dispatch']:.1f} GB/s over 32 dispatches); "
         f"one launch over all 32: {res['one_launch_32_matrices_GBps']:.1f} GB/s; one buffer repeated "
         f"(cache-warm): {tw * 1e6:.2f} us/GEMV")
+    res["roofline"] = row_roofline(res["GBps_per_dispatch"], "gemv_f16", bytes_one)
+    res["roofline_one_launch"] = row_roofline(res["one_launch_32_matrices_GBps"], "gemv_f16_one_launch",
+                                              bytes_one * cfg.rotate)
     if want_cpu:
         res["cpu_baseline"] = gemv_cpu_baseline(host_W, host_x, "f16", 2.0,
                                                 f"the 32 rotated {cfg.M} x {cfg.K} fp16 matrices in turn")
@@ -529,6 +549,18 @@ def row_protocol(stream, wsr, warmup_passes=12, passes=31, tokens=16, want_cpu=T
         replay()
         torch.cuda.synchronize()
         replays_ok &= all(torch.equal(a, d["y"][0]) for a, d in zip(eager, sp))
+    # the one-launch pass back to back (8 per event pair): the kernel's own rate, without the host's
+    # launch latency that a pass bracketed by its own synchronisation includes
+    for _ in range(warmup_passes):
+        one()
+    b2b = [timed(one, 8, stream) / 8 * 1e3 for _ in range(passes)]
+    st = spread(b2b)
+    res["one_launch_back_to_back"] = {"median_ms_per_pass": st["median"], "iqr_ms": st["iqr"],
+                                      "GBps_at_median": nbytes / (st["median"] * 1e-3) / 1e9,
+                                      "hbm_frac": nbytes / (st["median"] * 1e-3) / HBM_PEAK}
+    res["roofline"] = row_roofline(res["one_launch_back_to_back"]["GBps_at_median"], "protocol", nbytes)
+    log(f"protocol one launch, back to back: median {st['median'] * 1e3:.1f} us/pass, "
+        f"{res['one_launch_back_to_back']['GBps_at_median']:.1f} GB/s")
     for name, fn in (("dispatches_12", dispatches), ("one_launch", one), ("graph_12", replay)):
         for _ in range(warmup_passes):
             fn()

@@ -223,7 +223,9 @@ wsr_status wsr_decode_sweep_noalloc(const wsr_mat* mats, int32_t n, int32_t n_to
    product is exact and sums are fp32, but a slab's products are added in the matrix core's own
    order, so outputs agree with wsr_decode_sweep within rounding (not bit for bit); a unit
    activation vector still returns the dequantised weights exactly.  Tokens go in passes of 16, the
-   last pass holding the rest.  Formats, layouts, flags and the workspace as for wsr_decode_sweep;
+   last pass holding the rest.  A pass of a single token (n_tokens = 1, or a last pass of one) runs
+   the vector-ALU loop of wsr_decode_sweep instead, whose outputs it then equals bit for bit: a
+   matrix instruction would compute 16 token slots to use one.  Formats, layouts, flags and the workspace as for wsr_decode_sweep;
    with n_tokens > 1 every matrix must have y_tok_stride >= 4 M.  A row may hold at most 32 MiB of
    weights or codes and x_tok_stride may be at most 128 MiB (WSR_E_SIZE otherwise): the kernels
    address 64 rows and 16 tokens with 32-bit offsets. */

@@ -696,8 +696,15 @@ extern "C" wsr_status wsr_decode_sweep_mma(const wsr_mat* mats, int32_t n, int32
     DevMat* dtab = reinterpret_cast<DevMat*>(static_cast<char*>(ws) + wsr::SWEEP_CTR_BYTES);
     int64_t* dcost = reinterpret_cast<int64_t*>(reinterpret_cast<char*>(dtab) +
                                                 ((size_t)n * sizeof(DevMat) + 255) / 256 * 256);
-    hipError_t e = wsr::launch_put_table(dtab, dcost, p.tab.data(), n, ctr, s);
-    if (e != hipSuccess) return hip_fail(e, "decode_sweep_mma: table upload");
+    /* the matrix-core launches read the table from the workspace; a single-token pass may carry it
+       in its arguments */
+    bool upload = false;
+    for (int32_t t = 0; t < n_tokens && !upload; t += 16)
+        for (const Seg& g : p.segs)
+            upload |= std::min<int32_t>(16, n_tokens - t) > 1 || !wsr::sweep_table_by_value(g.count, g.total, g.fmt, 1);
+    hipError_t e = hipSuccess;
+    if (upload && (e = wsr::launch_put_table(dtab, dcost, p.tab.data(), n, ctr, s)) != hipSuccess)
+        return hip_fail(e, "decode_sweep_mma: table upload");
     std::vector<int64_t> max_group(p.segs.size(), 0), max_tail(p.segs.size(), 0);
     for (size_t i = 0; i < p.segs.size(); ++i)
         for (int m = p.segs[i].first; m < p.segs[i].first + p.segs[i].count; ++m) {
@@ -708,8 +715,12 @@ extern "C" wsr_status wsr_decode_sweep_mma(const wsr_mat* mats, int32_t n, int32
         const int ntok = std::min<int32_t>(16, n_tokens - t);
         for (size_t i = 0; i < p.segs.size(); ++i) {
             const Seg& g = p.segs[i];
-            e = wsr::launch_sweep_mma(dtab + g.first, dcost + g.first, g.count, g.total, max_group[i], max_tail[i], g.fmt,
-                                      t, ntok, s);
+            /* a pass of one token would fill 16 token slots of every matrix instruction for one; the
+               vector-ALU loop serves it instead (8B q4: 1.6k tok/s against 1.0k) */
+            e = ntok == 1 ? wsr::launch_sweep(dtab + g.first, dcost + g.first, p.tab.data() + g.first, g.count, g.total,
+                                              g.fmt, t, 1, ctr, s)
+                          : wsr::launch_sweep_mma(dtab + g.first, dcost + g.first, g.count, g.total, max_group[i],
+                                                  max_tail[i], g.fmt, t, ntok, s);
             if (e != hipSuccess) return hip_fail(e, "decode_sweep_mma: launch");
         }
     }

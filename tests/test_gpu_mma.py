@@ -66,7 +66,7 @@ def test_mma_unit_vectors_exact(fmt):
 
 
 @pytest.mark.parametrize("fmt", [wl.F16, wl.BF16, wl.Q4, wl.I8])
-@pytest.mark.parametrize("T", [1, 3, 16, 21])
+@pytest.mark.parametrize("T", [1, 3, 16, 17, 21])
 def test_mma_matrix_parity_and_bounds(fmt, T):
     """T tokens in passes of 16; rows in a strided output (gaps after each token's M rows) and the
     tokens past T stay NaN."""
@@ -242,3 +242,20 @@ def test_mma_mixed_full_size_tail():
             assert rel_l2(got, np.array(want)) <= TOL, (m.name, fmt, t)
     del inp, valu, mma
     torch.cuda.empty_cache()
+
+
+def test_mma_single_token_passes_equal_the_sweep():
+    """A pass of one token (n_tokens = 1, or the last of 17) runs the vector-ALU loop: those outputs
+    equal wsr_decode_sweep's bit for bit; the 16-token pass stays within rounding of them."""
+    mats = wl.decode_matrices(dv.small_model(layers=3, d=512, ffn=1536, vocab=3000))
+    fmts = [(wl.Q4, wl.BF16, wl.I8, wl.F16)[m.layer] for m in mats]
+    inp = dv.SweepInputs(mats, fmts, tokens=17)
+    valu, mma = sweep_pair(inp, 17)
+    for i in range(len(mats)):
+        a, b = valu[i].cpu().numpy(), mma[i].cpu().numpy()
+        assert np.array_equal(f32_bits(a[16]), f32_bits(b[16])), i
+        assert rel_l2(b[:16], a[:16]) <= MMA_VS_VALU, i
+    one = dv.SweepInputs([m for m, f in zip(mats, fmts) if f == wl.Q4], [wl.Q4] * 7, tokens=1)
+    valu, mma = sweep_pair(one, 1)
+    for a, b in zip(valu, mma):
+        assert np.array_equal(f32_bits(a.cpu().numpy()), f32_bits(b.cpu().numpy()))
