@@ -938,7 +938,7 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build measures one GPU: the weight-streaming path has no "
+        print(json.dumps({"error": "bench.py measures one GPU: the weight-streaming path has no "
                                    "multi-GPU form here (a sharded run would split rows across GPUs); "
                                    "run with --gpus 1"}))
         sys.exit(2)
