@@ -711,6 +711,14 @@ extern "C" wsr_status wsr_decode_sweep_mma(const wsr_mat* mats, int32_t n, int32
             max_group[i] = std::max(max_group[i], p.tab[m].row_bytes * std::min(p.tab[m].M, wsr::mma_group_rows()));
             max_tail[i] = std::max(max_tail[i], p.tab[m].row_bytes * std::min(p.tab[m].M, wsr::mma_tail_rows()));
         }
+    std::vector<int> mma_fmt(p.segs.size());
+    for (size_t i = 0; i < p.segs.size(); ++i) {
+        const Seg& g = p.segs[i];
+        bool whole = g.fmt == WSR_Q4;
+        for (int m = g.first; whole && m < g.first + g.count; ++m)
+            whole = p.tab[m].nc % 8 == 0 && (reinterpret_cast<uintptr_t>(p.tab[m].s) & 15) == 0;
+        mma_fmt[i] = whole ? wsr::FMT_Q4_WHOLE : g.fmt;
+    }
     for (int32_t t = 0; t < n_tokens; t += 16) {
         const int ntok = std::min<int32_t>(16, n_tokens - t);
         for (size_t i = 0; i < p.segs.size(); ++i) {
@@ -720,7 +728,7 @@ extern "C" wsr_status wsr_decode_sweep_mma(const wsr_mat* mats, int32_t n, int32
             e = ntok == 1 ? wsr::launch_sweep(dtab + g.first, dcost + g.first, p.tab.data() + g.first, g.count, g.total,
                                               g.fmt, t, 1, ctr, s)
                           : wsr::launch_sweep_mma(dtab + g.first, dcost + g.first, g.count, g.total, max_group[i],
-                                                  max_tail[i], g.fmt, t, ntok, s);
+                                                  max_tail[i], mma_fmt[i], t, ntok, s);
             if (e != hipSuccess) return hip_fail(e, "decode_sweep_mma: launch");
         }
     }

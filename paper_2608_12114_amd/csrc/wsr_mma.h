@@ -12,6 +12,7 @@
 #include <type_traits>
 
 #include "wsr_device.h"
+#include "wsr_mma_launch.h"
 
 namespace wsr {
 
@@ -128,8 +129,8 @@ template <int FMT> struct MmaStep { static constexpr int J = 2, SLABS = 2, K = 6
 template <> struct MmaStep<FMT_Q4> { static constexpr int J = 2, SLABS = 8, K = 256; };   /* 32 per chunk  */
 template <> struct MmaStep<FMT_I8> { static constexpr int J = 2, SLABS = 4, K = 128; };   /* 16 per chunk  */
 
-/* Registers of one unit (a group of NT tiles, one step): the activations of each slab, the chunks
-   of each tile, and the scales (q4: the step's eight block scales of each tile's row, as fp16
+/* Registers of one unit (a group of NT tiles, one step): the activations of each slab (16-bit and
+   int8; q4 keeps them in LDS), the chunks of each tile, and the scales (q4: the step's eight block scales of each tile's row, as fp16
    pairs; int8: each tile's row scale). */
 template <int FMT, int NT>
 struct MmaUnit {
@@ -182,11 +183,16 @@ __device__ __forceinline__ const char* uniform_ptr(const char* p) {
     return reinterpret_cast<const char*>(hi << 32 | lo);
 }
 
-/* q4 with rows of at least one step keeps the activations out of the register ring: each unit's
-   eight activation slabs go straight from memory into a two-unit ring in the wave's LDS
-   (xlds, 2 x 8 x 64 chunks of 16 bytes) and are read back slab by slab as they are multiplied. */
-template <int FMT, bool SHORT>
-constexpr bool mma_x_in_lds() { return FMT == FMT_Q4 && !SHORT; }
+/* q4 keeps the activations out of the register ring: each unit's eight activation slabs go
+   straight from memory into a two-unit ring in the wave's LDS and are read back slab by slab as
+   they are multiplied.  Where a step's eight block scales of a row are one aligned 16-byte run
+   (SCALE16), the unit's scales take a ninth slot of the ring: one load of 64 lanes brings the 16
+   bytes of each of the group's 64 rows, where loading them into registers took one instruction
+   per tile, each returning the same 16 bytes to all four lane groups (those loads cost a fifth of
+   the 16-token pass).  MMA_LDS_SLOTS is the ring's slots of 64 chunks of 16 bytes per unit. */
+template <int FMT>
+constexpr bool mma_x_in_lds() { return FMT == FMT_Q4; }
+constexpr int MMA_LDS_SLOTS = MmaStep<FMT_Q4>::SLABS + 1;
 
 /* Wait until at most n vector memory operations are outstanding (an LDS-DMA load's data is in LDS
    once it has left the count; operations leave it in the order they were issued). */
@@ -207,10 +213,10 @@ __device__ __forceinline__ void wait_vm() {
    arrive would make each load wait at once).  Rows shorter than one step (SHORT) clamp each
    lane's offset instead.  q4 reads a step's eight block scales as one 16-byte load where the rows
    hold a multiple of 8 blocks and the scales are 16-byte aligned (SCALE16); otherwise one by one.
-   The caller keeps 16 NT rows of codes and 16 tokens of activations within 2^31 bytes.  q4 rows of
-   at least one step take their activations from the LDS ring (mma_x_in_lds), which leaves the
-   register ring to the weights and scales: at 16 tokens on the 8B model 13.7k -> 14.1k tok/s, and
-   974 -> 1043 tok/s at one token. */
+   The caller keeps 16 NT rows of codes and 16 tokens of activations within 2^31 bytes.  q4 takes
+   its activations (and, with SCALE16, its scales) from the LDS ring (mma_x_in_lds), which leaves
+   the register ring to the weights: at 16 tokens on the 8B model 13.7k -> 14.1k tok/s with the
+   activations there, 13.7k -> 15.3k once they arrive as whole lines and the scales join them. */
 template <int FMT, int NT, bool SCALE16, bool SHORT>
 __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1, int32_t token0, int ntok, int lane,
                                          u32x4* __restrict__ xlds) {
@@ -236,6 +242,22 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
     int lbuf = 0, mbuf = 0;                                      /* LDS ring half of the next load, multiply */
     rsrc_t rw = buffer_of(d.w), rs = buffer_of(d.w);             /* this group's row r0 of codes, scales */
     uint32_t vr[NT], vs[NT];                                     /* lane offsets: row of each tile */
+    uint32_t vsd = 0;                                            /* the row of lane i % 16 NT (scales to LDS) */
+    /* q4 activations reach LDS as whole 128-byte lines: load q of a unit (slab pair p = q / 2, token
+       half h = q % 2) gives lane i token 8 h + i / 8 at chunk (i % 8) ^ (i / 8) of its line holding
+       slabs 2 p and 2 p + 1.  The chunks are stored rotated by token so that the slab reads, 16
+       tokens of one chunk per lane group, spread over the LDS banks.  Lane (c, g) reads slab s at
+       slot 128 (s / 2) + rd[s % 2] of the ring. */
+    const int xi = lane >> 3, xc = (lane & 7) ^ xi;
+    uint32_t xt[2];                                              /* the token row of each half */
+#pragma unroll
+    for (int h = 0; h < 2; ++h) xt[h] = (uint32_t)((8 * h + xi < ntok ? 8 * h + xi : 0) * d.x_stride);
+    int rd[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) rd[e] = (c >> 3) * WAVE + (c & 7) * 8 + ((4 * e + g) ^ (c & 7));
+    constexpr bool S_LDS = FMT == FMT_Q4 && SCALE16;
+    constexpr int NDMA = SL + (S_LDS ? 1 : 0);                   /* loads into LDS per unit */
+    static_assert(!mma_x_in_lds<FMT>() || NDMA <= MMA_LDS_SLOTS, "LDS ring slots");
     uint32_t vh[NT];                                             /* the row of the tile's second half */
     const uint32_t lc = 16 * (g + 4 * (c >> 3));                 /* the lane's byte within a 128-byte line */
     static_assert(J == 2, "a step is one line of each row");
@@ -252,47 +274,49 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
                 vr[t] = (uint32_t)((std::min<int64_t>(i0 + 16 * t + (c & 7), r1 - 1) - i0) * crb);
                 vh[t] = (uint32_t)((std::min<int64_t>(i0 + 16 * t + 8 + (c & 7), r1 - 1) - i0) * crb);
             }
+            if constexpr (S_LDS) vsd = (uint32_t)((std::min<int64_t>(i0 + lane % (16 * NT), r1 - 1) - i0) * srow);
         }
-        if constexpr (!SHORT) {
-            /* the last step ends at the row's end; offsets stay below 2^31 (the caller's limits) */
-            const uint32_t kb = (uint32_t)std::min<int64_t>((int64_t)kl * SB, crb - SB);
-            const uint32_t xo = (uint32_t)(std::min<int64_t>((int64_t)kl * SK, kelem - SK) * 2);
-            if constexpr (mma_x_in_lds<FMT, SHORT>()) {
-                /* the slabs first, so that every load issued after them is counted by wait_vm */
-                u32x4* ring = xlds + (lbuf ? SL * WAVE : 0);
-#pragma unroll
-                for (int s = 0; s < SL; ++s) buf_to_lds(rx, ring + s * WAVE, vx + mma_x_byte<FMT>(s), xo);
-                lbuf ^= 1;
-                __builtin_amdgcn_sched_barrier(0);
-            }
-#pragma unroll
-            for (int t = 0; t < NT; ++t)
-#pragma unroll
-                for (int jj = 0; jj < J; ++jj) u.w[t][jj] = buf_once(rw, (jj ? vh[t] : vr[t]) + lc, kb);
-            if constexpr (!mma_x_in_lds<FMT, SHORT>()) {
-#pragma unroll
-                for (int s = 0; s < SL; ++s) u.x[s] = buf_reused(rx, vx + mma_x_byte<FMT>(s), xo);
-            }
-        } else {                                                 /* one step, shorter than SB: clamp per lane */
-#pragma unroll
-            for (int t = 0; t < NT; ++t)
-#pragma unroll
-                for (int jj = 0; jj < J; ++jj)
-                    u.w[t][jj] = buf_once(rw, (jj ? vh[t] : vr[t]) + (uint32_t)std::min<int64_t>(lc, crb - 16), 0);
-#pragma unroll
-            for (int s = 0; s < SL; ++s) {
+        /* the last step ends at the row's end; offsets stay below 2^31 (the caller's limits) */
+        const uint32_t kb = SHORT ? 0 : (uint32_t)std::min<int64_t>((int64_t)kl * SB, crb - SB);
+        const uint32_t xo = SHORT ? 0 : (uint32_t)(std::min<int64_t>((int64_t)kl * SK, kelem - SK) * 2);
+        /* lane offset of slab s's activations; a row shorter than one step clamps them per lane */
+        auto x_off = [&](int s) -> uint32_t {
+            if constexpr (SHORT) {
                 const int64_t e = std::min<int64_t>((XG * g + mma_x_byte<FMT>(s)) / 2, kelem - 8);
-                u.x[s] = buf_reused(rx, vx - XG * g + (uint32_t)(2 * e), 0);
+                return vx - XG * g + (uint32_t)(2 * e);
+            } else {
+                return vx + mma_x_byte<FMT>(s);
             }
+        };
+        const uint32_t b0 = SHORT ? 0 : (uint32_t)std::min<int64_t>((int64_t)kl * 8, nc - 8);   /* q4: first block */
+        if constexpr (mma_x_in_lds<FMT>()) {
+            /* the slabs (and scales) first, so that every load issued after them is counted by wait_vm */
+            u32x4* ring = xlds + (lbuf ? NDMA * WAVE : 0);
+#pragma unroll
+            for (int q = 0; q < SL; ++q) {
+                const int p = q >> 1, h = q & 1;
+                const uint32_t v = SHORT ? xt[h] + 2 * (uint32_t)std::min<int64_t>(64 * p + 8 * xc, kelem - 8)
+                                         : xt[h] + 16 * xc + 128 * p;
+                buf_to_lds(rx, ring + q * WAVE, v, xo);
+            }
+            if constexpr (S_LDS) buf_to_lds(rs, ring + SL * WAVE, vsd, b0 * 2);
+            lbuf ^= 1;
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        /* a row shorter than one step clamps each lane's weight offset */
+        const uint32_t lw = SHORT ? (uint32_t)std::min<int64_t>(lc, crb - 16) : lc;
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+            for (int jj = 0; jj < J; ++jj) u.w[t][jj] = buf_once(rw, (jj ? vh[t] : vr[t]) + lw, kb);
+        if constexpr (!mma_x_in_lds<FMT>()) {
+#pragma unroll
+            for (int s = 0; s < SL; ++s) u.x[s] = buf_reused(rx, x_off(s), xo);
         }
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             if constexpr (FMT == FMT_Q4) {
-                const uint32_t b0 = SHORT ? 0 : (uint32_t)std::min<int64_t>((int64_t)kl * 8, nc - 8);   /* first block */
-                if constexpr (SCALE16) {
-                    const u32x4 v = buf_reused(rs, vs[t], b0 * 2);
-                    u.s[t][0] = v.x, u.s[t][1] = v.y, u.s[t][2] = v.z, u.s[t][3] = v.w;
-                } else {
+                if constexpr (!SCALE16) {                        /* (SCALE16: in the LDS ring) */
                     uint32_t h[8];
 #pragma unroll
                     for (int j = 0; j < 8; ++j) h[j] = buf_u16(rs, vs[t], (uint32_t)std::min<int64_t>(b0 + j, nc - 1) * 2);
@@ -305,16 +329,16 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
         }
         if (++kl == steps) { kl = 0; ++gl; }
     };
-    /* Vector memory operations each load() issues after its activation slabs (weights, scales). */
-    constexpr int AFTER_X = NT * J + (FMT == FMT_Q4 ? (SCALE16 ? NT : 8 * NT) : 0);
-    constexpr int PER_UNIT = SL + AFTER_X;
+    /* Vector memory operations each load() issues after its loads into LDS (weights, scales). */
+    constexpr int AFTER_X = NT * J + (FMT == FMT_Q4 ? (SCALE16 ? 0 : 8 * NT) : 0);
+    constexpr int PER_UNIT = NDMA + AFTER_X;
     auto multiply = [&](Unit& u, auto next_loaded) {
         const int64_t i0 = r0 + gc * 16 * NT;
         /* the step's first weight, and the first one it has not already covered */
         const int64_t e0 = SHORT ? 0 : std::min<int64_t>((int64_t)kc * SK, kelem - SK), e1 = SHORT ? 0 : (int64_t)kc * SK;
 #pragma unroll
         for (int t = 0; t < NT; ++t) lines_to_slabs(u.w[t][0], u.w[t][1]);
-        if constexpr (mma_x_in_lds<FMT, SHORT>()) {
+        if constexpr (mma_x_in_lds<FMT>()) {
 #pragma unroll
             for (int t = 0; t < NT; ++t)
 #pragma unroll
@@ -323,30 +347,56 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
             constexpr int AFTER = AFTER_X + (decltype(next_loaded)::value ? PER_UNIT : 0);
             wait_vm<(AFTER < 63 ? AFTER : 63)>();
             __builtin_amdgcn_sched_barrier(0);
-            const u32x4* ring = xlds + (mbuf ? SL * WAVE : 0) + lane;
+            const u32x4* ring = xlds + (mbuf ? NDMA * WAVE : 0);
             mbuf ^= 1;
-            const bool moved = e0 < e1;                          /* a moved-back last step */
+            if constexpr (S_LDS) {                               /* lane (c, g): row c of each tile */
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    const u32x4 v = ring[SL * WAVE + 16 * t + c];
+                    u.s[t][0] = v.x, u.s[t][1] = v.y, u.s[t][2] = v.z, u.s[t][3] = v.w;
+                }
+            }
+            const bool masked = SHORT || e0 < e1;                /* a short row or a moved-back last step */
+            /* Each slab's products are scaled and summed while the next slab's matrix instructions
+               run, and the sum is pinned there: left alone, the compiler sinks every scaled sum to
+               the end of the unit and keeps all 32 products live (128 registers, one wave per SIMD
+               instead of two). */
+            f4_t pend[NT];
+            float psc[NT];
 #pragma unroll
             for (int sl = 0; sl < SL; ++sl) {                   /* slab sl: block e0 / 32 + sl of each row */
-                u32x4 xs = ring[sl * WAVE];
-                if (__builtin_expect(moved, 0)) {
+                u32x4 xs = ring[(sl >> 1) * 2 * WAVE + rd[sl & 1]];
+                if (__builtin_expect(masked, 0)) {
                     const int64_t e = e0 + (XG * g + mma_x_byte<FMT>(sl)) / 2;
                     xs = keep_if(e >= e1 && e < kelem, xs);
                 }
                 xs = x8_q4_order(xs);
+                f4_t p[NT];
+#pragma unroll
+                for (int t = 0; t < NT; ++t)
+                    p[t] = mma16<FMT_F16>(xs, q4_word_f16(u.w[t][sl / 4][sl % 4]), f4_t{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
                 for (int t = 0; t < NT; ++t) {
+                    if (sl > 0) {
+                        acc[t] += psc[t] * pend[t];
+                        __asm__ volatile("" : "+v"(acc[t]));
+                    }
                     float sc = f16_bits_to_f32((uint16_t)(u.s[t][sl / 2] >> (16 * (sl % 2))));
                     if constexpr (!SCALE16) {
                         const int64_t b = e0 / 32 + sl;
                         sc = b >= e1 / 32 && b < nc ? sc : 0.f;
                     }
-                    const f4_t p = mma16<FMT_F16>(xs, q4_word_f16(u.w[t][sl / 4][sl % 4]), f4_t{0.f, 0.f, 0.f, 0.f});
-                    acc[t] += sc * p;
+                    pend[t] = p[t];
+                    psc[t] = sc;
                 }
-                __builtin_amdgcn_sched_barrier(0);               /* one slab's values live at a time */
+                __builtin_amdgcn_sched_barrier(0);               /* two slabs' values live at a time */
             }
-        } else {
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                acc[t] += psc[t] * pend[t];
+                __asm__ volatile("" : "+v"(acc[t]));
+            }
+        } else {                                                 /* 16-bit and int8: activations in registers */
         if (__builtin_expect(SHORT || e0 < e1, 0)) {             /* a moved-back or short last step */
             __asm__ volatile("" ::: "memory");                   /* kept a branch, not selects run every step */
 #pragma unroll
@@ -354,7 +404,7 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
                 const int64_t e = e0 + (XG * g + mma_x_byte<FMT>(s)) / 2;
                 u.x[s] = keep_if(e >= e1 && e < kelem, u.x[s]);
             }
-            if constexpr (FMT != FMT_Q4 && FMT != FMT_I8) {     /* 16-bit weights there may not be finite */
+            if constexpr (FMT != FMT_I8) {                       /* 16-bit weights there may not be finite */
 #pragma unroll
                 for (int t = 0; t < NT; ++t)
 #pragma unroll
@@ -366,24 +416,7 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
         }
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            if constexpr (FMT == FMT_Q4) {
-#pragma unroll
-                for (int jj = 0; jj < J; ++jj) {
-                    const u32x4 w = transpose_groups(u.w[t][jj]);
-                    const uint32_t wj[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {                /* block e0 / 32 + s of the row */
-                        const int s = 4 * jj + j;
-                        float sc = f16_bits_to_f32((uint16_t)(u.s[t][s / 2] >> (16 * (s % 2))));
-                        if constexpr (!SCALE16) {                /* blocks outside the step's new part */
-                            const int64_t b = e0 / 32 + s;
-                            sc = b >= e1 / 32 && b < nc ? sc : 0.f;
-                        }
-                        const f4_t p = mma16<FMT_F16>(x8_q4_order(u.x[s]), q4_word_f16(wj[j]), f4_t{0.f, 0.f, 0.f, 0.f});
-                        acc[t] += sc * p;
-                    }
-                }
-            } else if constexpr (FMT == FMT_I8) {
+            if constexpr (FMT == FMT_I8) {
 #pragma unroll
                 for (int jj = 0; jj < J; ++jj) {
                     acc[t] = mma16<FMT_F16>(x8_i8_order(u.x[2 * jj]), i8_words_f16(u.w[t][jj].x, u.w[t][jj].y), acc[t]);
@@ -440,6 +473,8 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
     }
 }
 
+constexpr int mma_base_fmt(int fmt) { return fmt == FMT_Q4_WHOLE ? FMT_Q4 : fmt; }
+
 /* The matrix-core sweep over the byte range [lo, hi) of the weight stream (groups of 16 NT rows). */
 template <int FMT, int NT>
 __device__ __forceinline__ void stream_range_mma(const DevMat* __restrict__ tab, const int64_t* __restrict__ cost,
@@ -449,7 +484,8 @@ __device__ __forceinline__ void stream_range_mma(const DevMat* __restrict__ tab,
         const DevMat d = tab[m];
         if (d.cost0 >= hi) break;
         hint = m;
-        const int fmt = FMT ? FMT : d.fmt;
+        constexpr int F = mma_base_fmt(FMT);
+        const int fmt = F ? F : d.fmt;
         RowRange rr = range_rows(d, lo, hi, 16 * NT);
         if (tail > 0) {              /* rows below the main region's last boundary are not the tail's */
             const int64_t fl = tail > d.cost0 ? ceil_div(tail - d.cost0, d.row_bytes * main_rows) * main_rows : 0;
@@ -460,15 +496,17 @@ __device__ __forceinline__ void stream_range_mma(const DevMat* __restrict__ tab,
         if (rr.r0 >= rr.r1) continue;
         const bool short_rows = d.nc * 16 < 128;                 /* under one step */
 #define WSR_ROWS(F, S16, SH) rows_mma<F, NT, S16, SH>(d, rr.r0, rr.r1, token0, ntok, lane, xlds)
-        if ((FMT == 0 || FMT == FMT_F16) && fmt == FMT_F16) {
+        if constexpr (FMT == FMT_Q4_WHOLE) {                     /* the launcher checked every matrix */
+            WSR_ROWS(FMT_Q4, true, false);
+        } else if ((F == 0 || F == FMT_F16) && fmt == FMT_F16) {
             if (short_rows) WSR_ROWS(FMT_F16, false, true); else WSR_ROWS(FMT_F16, false, false);
-        } else if ((FMT == 0 || FMT == FMT_BF16) && fmt == FMT_BF16) {
+        } else if ((F == 0 || F == FMT_BF16) && fmt == FMT_BF16) {
             if (short_rows) WSR_ROWS(FMT_BF16, false, true); else WSR_ROWS(FMT_BF16, false, false);
-        } else if ((FMT == 0 || FMT == FMT_Q4) && fmt == FMT_Q4) {
+        } else if ((F == 0 || F == FMT_Q4) && fmt == FMT_Q4) {
             if (short_rows) WSR_ROWS(FMT_Q4, false, true);
             else if (d.nc % 8 == 0 && (reinterpret_cast<uintptr_t>(d.s) & 15) == 0) WSR_ROWS(FMT_Q4, true, false);
             else WSR_ROWS(FMT_Q4, false, false);
-        } else if ((FMT == 0 || FMT == FMT_I8) && fmt == FMT_I8) {
+        } else if ((F == 0 || F == FMT_I8) && fmt == FMT_I8) {
             if (short_rows) WSR_ROWS(FMT_I8, false, true); else WSR_ROWS(FMT_I8, false, false);
         }
 #undef WSR_ROWS

@@ -39,8 +39,8 @@ __global__ __launch_bounds__(WAVE) void k_sweep_mma(const DevMat* __restrict__ t
     const int64_t hi = base + q * (k + 1) + (int64_t)((uint64_t)r * (uint64_t)(k + 1) / nw);
     int hint = 0;
     if (lo >= hi) return;
-    /* the q4 activation ring: two units of 8 slabs of 64 16-byte chunks (16 KiB) */
-    __shared__ u32x4 xlds[2 * MmaStep<FMT_Q4>::SLABS * WAVE];
+    /* the q4 ring: two units of 8 activation slabs and the scales, 64 16-byte chunks each (18 KiB) */
+    __shared__ u32x4 xlds[2 * MMA_LDS_SLOTS * WAVE];
     if (main)
         stream_range_mma<FMT, MMA_TILES>(tab, cost, nmat, lo, hi, 0, 16 * MMA_TILES, token0, ntok, lane, hint, xlds);
     else
@@ -55,11 +55,11 @@ int64_t mma_tail_rows() { return 16 * MMA_TAIL_TILES; }
    found once per device and format. */
 static hipError_t mma_slots(int fmt_all, int64_t& slots) {
     static std::mutex mu;
-    static int64_t cache[64][5] = {};
+    static int64_t cache[64][9] = {};
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
-    const int f = fmt_all >= 0 && fmt_all <= 4 ? fmt_all : 0;
+    const int f = (fmt_all >= 0 && fmt_all <= 4) || fmt_all == FMT_Q4_WHOLE ? fmt_all : 0;
     std::lock_guard<std::mutex> lock(mu);
     if (dev >= 0 && dev < 64 && cache[dev][f] > 0) {
         slots = cache[dev][f];
@@ -72,6 +72,9 @@ static hipError_t mma_slots(int fmt_all, int64_t& slots) {
         case FMT_BF16: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_sweep_mma<FMT_BF16>, WAVE, 0); break;
         case FMT_Q4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_sweep_mma<FMT_Q4>, WAVE, 0); break;
         case FMT_I8: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_sweep_mma<FMT_I8>, WAVE, 0); break;
+        case FMT_Q4_WHOLE:
+            e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_sweep_mma<FMT_Q4_WHOLE>, WAVE, 0);
+            break;
         default: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_sweep_mma<0>, WAVE, 0); break;
     }
     if (e != hipSuccess) return e;
@@ -110,6 +113,7 @@ hipError_t launch_sweep_mma(const DevMat* tab, const int64_t* cost, int nmat, in
         case FMT_BF16: WSR_MMA(FMT_BF16); break;
         case FMT_Q4: WSR_MMA(FMT_Q4); break;
         case FMT_I8: WSR_MMA(FMT_I8); break;
+        case FMT_Q4_WHOLE: WSR_MMA(FMT_Q4_WHOLE); break;
         default: WSR_MMA(0); break;
     }
 #undef WSR_MMA

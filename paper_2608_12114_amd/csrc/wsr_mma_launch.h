@@ -8,6 +8,12 @@
 
 namespace wsr {
 
+/* The kernel format of a q4 table whose every matrix reads a step's eight block scales as one
+   16-byte load: rows of a whole number of 8-block steps (nc % 8 == 0) and 16-byte aligned scales.
+   Its kernel holds only that loop, which fits two waves per SIMD (255 registers, against 280 for
+   the kernel with every q4 loop). */
+constexpr int FMT_Q4_WHOLE = 8;
+
 /* Tokens token0 .. token0 + ntok - 1 (ntok <= 16) of the sweep on the matrix cores; max_group and
    max_tail_group are the largest row group's weight-stream bytes (mma_group_rows() rows, and
    mma_tail_rows() rows for the tail of the stream, of any matrix in the table). */
