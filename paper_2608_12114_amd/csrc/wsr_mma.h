@@ -129,14 +129,13 @@ template <int FMT> struct MmaStep { static constexpr int J = 2, SLABS = 2, K = 6
 template <> struct MmaStep<FMT_Q4> { static constexpr int J = 2, SLABS = 8, K = 256; };   /* 32 per chunk  */
 template <> struct MmaStep<FMT_I8> { static constexpr int J = 2, SLABS = 4, K = 128; };   /* 16 per chunk  */
 
-/* Registers of one unit (a group of NT tiles, one step): the activations of each slab (16-bit and
-   int8; q4 keeps them in LDS), the chunks of each tile, and the scales (q4: the step's eight block scales of each tile's row, as fp16
-   pairs; int8: each tile's row scale). */
+/* Registers of one unit (a group of NT tiles, one step): the chunks of each tile and the scales
+   (q4: the step's eight block scales of each tile's row, as fp16 pairs; int8: each tile's row
+   scale).  The activations go through LDS. */
 template <int FMT, int NT>
 struct MmaUnit {
     static constexpr int J = MmaStep<FMT>::J, SL = MmaStep<FMT>::SLABS;
     static constexpr int NS = FMT == FMT_Q4 ? 4 : 1;
-    u32x4 x[SL];
     u32x4 w[NT][J];
     uint32_t s[NT][NS];
 };
@@ -161,9 +160,6 @@ __device__ __forceinline__ rsrc_t buffer_of(const void* base) {
 __device__ __forceinline__ u32x4 buf_once(rsrc_t r, uint32_t v, uint32_t s) {
     return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, v, s, 2));
 }
-__device__ __forceinline__ u32x4 buf_reused(rsrc_t r, uint32_t v, uint32_t s) {
-    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, v, s, 0));
-}
 __device__ __forceinline__ uint32_t buf_u16(rsrc_t r, uint32_t v, uint32_t s) {
     return __builtin_amdgcn_raw_buffer_load_b16(r, v, s, 0);
 }
@@ -183,16 +179,16 @@ __device__ __forceinline__ const char* uniform_ptr(const char* p) {
     return reinterpret_cast<const char*>(hi << 32 | lo);
 }
 
-/* q4 keeps the activations out of the register ring: each unit's eight activation slabs go
-   straight from memory into a two-unit ring in the wave's LDS and are read back slab by slab as
-   they are multiplied.  Where a step's eight block scales of a row are one aligned 16-byte run
-   (SCALE16), the unit's scales take a ninth slot of the ring: one load of 64 lanes brings the 16
+/* The activations stay out of the register ring: each unit's activation slabs go straight from
+   memory into a two-unit ring in the wave's LDS and are read back slab by slab as they are
+   multiplied (8B q4 at 16 tokens 13.7k -> 14.1k tok/s, int8 protocol 74.7k -> 80.8k, 70B bf16
+   +0.5 to +0.9 %).  Where a step's eight q4 block scales of a row are one aligned 16-byte run
+   (SCALE16), the unit's scales take one more slot of the ring: one load of 64 lanes brings the 16
    bytes of each of the group's 64 rows, where loading them into registers took one instruction
-   per tile, each returning the same 16 bytes to all four lane groups (those loads cost a fifth of
-   the 16-token pass).  MMA_LDS_SLOTS is the ring's slots of 64 chunks of 16 bytes per unit. */
+   per tile, each returning the same 16 bytes to all four lane groups.  mma_ring_slots is the
+   ring's slots of 64 chunks of 16 bytes per unit (0: no ring). */
 template <int FMT>
-constexpr bool mma_x_in_lds() { return FMT == FMT_Q4; }
-constexpr int MMA_LDS_SLOTS = MmaStep<FMT_Q4>::SLABS + 1;
+constexpr int mma_ring_slots() { return FMT == FMT_Q4 ? MmaStep<FMT_Q4>::SLABS + 1 : MmaStep<FMT>::SLABS; }
 
 /* Wait until at most n vector memory operations are outstanding (an LDS-DMA load's data is in LDS
    once it has left the count; operations leave it in the order they were issued). */
@@ -213,10 +209,9 @@ __device__ __forceinline__ void wait_vm() {
    arrive would make each load wait at once).  Rows shorter than one step (SHORT) clamp each
    lane's offset instead.  q4 reads a step's eight block scales as one 16-byte load where the rows
    hold a multiple of 8 blocks and the scales are 16-byte aligned (SCALE16); otherwise one by one.
-   The caller keeps 16 NT rows of codes and 16 tokens of activations within 2^31 bytes.  q4 takes
-   its activations (and, with SCALE16, its scales) from the LDS ring (mma_x_in_lds), which leaves
-   the register ring to the weights: at 16 tokens on the 8B model 13.7k -> 14.1k tok/s with the
-   activations there, 13.7k -> 15.3k once they arrive as whole lines and the scales join them. */
+   The caller keeps 16 NT rows of codes and 16 tokens of activations within 2^31 bytes.  The
+   activations (and, with SCALE16, the q4 scales) come from the LDS ring, which leaves the register
+   ring to the weights. */
 template <int FMT, int NT, bool SCALE16, bool SHORT>
 __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1, int32_t token0, int ntok, int lane,
                                          u32x4* __restrict__ xlds) {
@@ -232,7 +227,6 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
     const int64_t n = ngroups * steps;                           /* units */
     if (n == 0) return;
     const rsrc_t rx = buffer_of(uniform_ptr(static_cast<const char*>(d.x) + (int64_t)token0 * d.x_stride));
-    const uint32_t vx = (uint32_t)((c < ntok ? c : 0) * d.x_stride) + XG * g;
     const int64_t srow = FMT == FMT_Q4 ? nc * 2 : 2;             /* scale bytes per row */
     f4_t acc[NT];
 #pragma unroll
@@ -243,21 +237,24 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
     rsrc_t rw = buffer_of(d.w), rs = buffer_of(d.w);             /* this group's row r0 of codes, scales */
     uint32_t vr[NT], vs[NT];                                     /* lane offsets: row of each tile */
     uint32_t vsd = 0;                                            /* the row of lane i % 16 NT (scales to LDS) */
-    /* q4 activations reach LDS as whole 128-byte lines: load q of a unit (slab pair p = q / 2, token
-       half h = q % 2) gives lane i token 8 h + i / 8 at chunk (i % 8) ^ (i / 8) of its line holding
-       slabs 2 p and 2 p + 1.  The chunks are stored rotated by token so that the slab reads, 16
+    /* Ring activations reach LDS as whole 128-byte lines: load q of a unit (line p = q / 2 of the
+       step, token half h = q % 2) gives lane i token 8 h + i / 8 at chunk (i % 8) ^ (i / 8) of line
+       p, which holds slabs 2 p and 2 p + 1 (q4: chunk 4 (s % 2) + g of slab s for lane group g;
+       int8: chunk s % 2 + 2 g).  The chunks are stored rotated by token so that the slab reads, 16
        tokens of one chunk per lane group, spread over the LDS banks.  Lane (c, g) reads slab s at
-       slot 128 (s / 2) + rd[s % 2] of the ring. */
+       slot 128 (s / 2) + rd[s % 2] of the ring.  Whole lines halve the cache lines each load
+       touches (8B q4 at 16 tokens: 13.9k -> 15.3k tok/s). */
     const int xi = lane >> 3, xc = (lane & 7) ^ xi;
     uint32_t xt[2];                                              /* the token row of each half */
 #pragma unroll
     for (int h = 0; h < 2; ++h) xt[h] = (uint32_t)((8 * h + xi < ntok ? 8 * h + xi : 0) * d.x_stride);
     int rd[2];
 #pragma unroll
-    for (int e = 0; e < 2; ++e) rd[e] = (c >> 3) * WAVE + (c & 7) * 8 + ((4 * e + g) ^ (c & 7));
+    for (int e = 0; e < 2; ++e)
+        rd[e] = (c >> 3) * WAVE + (c & 7) * 8 + ((FMT == FMT_I8 ? e + 2 * g : 4 * e + g) ^ (c & 7));
     constexpr bool S_LDS = FMT == FMT_Q4 && SCALE16;
     constexpr int NDMA = SL + (S_LDS ? 1 : 0);                   /* loads into LDS per unit */
-    static_assert(!mma_x_in_lds<FMT>() || NDMA <= MMA_LDS_SLOTS, "LDS ring slots");
+    static_assert(NDMA <= mma_ring_slots<FMT>(), "LDS ring slots");
     uint32_t vh[NT];                                             /* the row of the tile's second half */
     const uint32_t lc = 16 * (g + 4 * (c >> 3));                 /* the lane's byte within a 128-byte line */
     static_assert(J == 2, "a step is one line of each row");
@@ -279,18 +276,10 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
         /* the last step ends at the row's end; offsets stay below 2^31 (the caller's limits) */
         const uint32_t kb = SHORT ? 0 : (uint32_t)std::min<int64_t>((int64_t)kl * SB, crb - SB);
         const uint32_t xo = SHORT ? 0 : (uint32_t)(std::min<int64_t>((int64_t)kl * SK, kelem - SK) * 2);
-        /* lane offset of slab s's activations; a row shorter than one step clamps them per lane */
-        auto x_off = [&](int s) -> uint32_t {
-            if constexpr (SHORT) {
-                const int64_t e = std::min<int64_t>((XG * g + mma_x_byte<FMT>(s)) / 2, kelem - 8);
-                return vx - XG * g + (uint32_t)(2 * e);
-            } else {
-                return vx + mma_x_byte<FMT>(s);
-            }
-        };
         const uint32_t b0 = SHORT ? 0 : (uint32_t)std::min<int64_t>((int64_t)kl * 8, nc - 8);   /* q4: first block */
-        if constexpr (mma_x_in_lds<FMT>()) {
-            /* the slabs (and scales) first, so that every load issued after them is counted by wait_vm */
+        {
+            /* the slabs (and scales) first, so that every load issued after them is counted by
+               wait_vm; a row shorter than one step clamps each lane's activation offset */
             u32x4* ring = xlds + (lbuf ? NDMA * WAVE : 0);
 #pragma unroll
             for (int q = 0; q < SL; ++q) {
@@ -309,10 +298,6 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
         for (int t = 0; t < NT; ++t)
 #pragma unroll
             for (int jj = 0; jj < J; ++jj) u.w[t][jj] = buf_once(rw, (jj ? vh[t] : vr[t]) + lw, kb);
-        if constexpr (!mma_x_in_lds<FMT>()) {
-#pragma unroll
-            for (int s = 0; s < SL; ++s) u.x[s] = buf_reused(rx, x_off(s), xo);
-        }
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             if constexpr (FMT == FMT_Q4) {
@@ -324,12 +309,14 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
                     for (int j = 0; j < 4; ++j) u.s[t][j] = h[2 * j] | h[2 * j + 1] << 16;
                 }
             } else if constexpr (FMT == FMT_I8) {
-                u.s[t][0] = buf_u16(rs, vs[t], 0);
+                if (kl + 1 == steps) u.s[t][0] = buf_u16(rs, vs[t], 0);   /* read only by the group's last step */
             }
         }
         if (++kl == steps) { kl = 0; ++gl; }
     };
-    /* Vector memory operations each load() issues after its loads into LDS (weights, scales). */
+    /* Vector memory operations each load() issues after its loads into LDS (weights, scales; the
+       int8 row scales, loaded on a group's last step only, are left out: a wait that counts fewer
+       later loads than were issued still covers the ring). */
     constexpr int AFTER_X = NT * J + (FMT == FMT_Q4 ? (SCALE16 ? 0 : 8 * NT) : 0);
     constexpr int PER_UNIT = NDMA + AFTER_X;
     auto multiply = [&](Unit& u, auto next_loaded) {
@@ -338,11 +325,13 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
         const int64_t e0 = SHORT ? 0 : std::min<int64_t>((int64_t)kc * SK, kelem - SK), e1 = SHORT ? 0 : (int64_t)kc * SK;
 #pragma unroll
         for (int t = 0; t < NT; ++t) lines_to_slabs(u.w[t][0], u.w[t][1]);
-        if constexpr (mma_x_in_lds<FMT>()) {
+        {
+            if constexpr (FMT == FMT_Q4) {
 #pragma unroll
-            for (int t = 0; t < NT; ++t)
+                for (int t = 0; t < NT; ++t)
 #pragma unroll
-                for (int jj = 0; jj < J; ++jj) u.w[t][jj] = transpose_groups(u.w[t][jj]);
+                    for (int jj = 0; jj < J; ++jj) u.w[t][jj] = transpose_groups(u.w[t][jj]);
+            }
             /* the unit's slabs are in LDS once no more than the loads issued after them remain */
             constexpr int AFTER = AFTER_X + (decltype(next_loaded)::value ? PER_UNIT : 0);
             wait_vm<(AFTER < 63 ? AFTER : 63)>();
@@ -357,76 +346,78 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
                 }
             }
             const bool masked = SHORT || e0 < e1;                /* a short row or a moved-back last step */
-            /* Each slab's products are scaled and summed while the next slab's matrix instructions
-               run, and the sum is pinned there: left alone, the compiler sinks every scaled sum to
-               the end of the unit and keeps all 32 products live (128 registers, one wave per SIMD
-               instead of two). */
-            f4_t pend[NT];
-            float psc[NT];
-#pragma unroll
-            for (int sl = 0; sl < SL; ++sl) {                   /* slab sl: block e0 / 32 + sl of each row */
+            auto slab = [&](int sl) -> u32x4 {
                 u32x4 xs = ring[(sl >> 1) * 2 * WAVE + rd[sl & 1]];
                 if (__builtin_expect(masked, 0)) {
                     const int64_t e = e0 + (XG * g + mma_x_byte<FMT>(sl)) / 2;
                     xs = keep_if(e >= e1 && e < kelem, xs);
                 }
-                xs = x8_q4_order(xs);
-                f4_t p[NT];
+                return xs;
+            };
+            if constexpr (FMT != FMT_Q4 && FMT != FMT_I8) {       /* 16-bit */
+                if (__builtin_expect(masked, 0)) {               /* 16-bit weights there may not be finite */
+#pragma unroll
+                    for (int t = 0; t < NT; ++t)
+#pragma unroll
+                        for (int jj = 0; jj < J; ++jj) {
+                            const int64_t e = e0 + 32 * jj + 8 * g;
+                            u.w[t][jj] = keep_if(e >= e1 && e < kelem, u.w[t][jj]);
+                        }
+                }
+                u32x4 xs[SL];
+#pragma unroll
+                for (int sl = 0; sl < SL; ++sl) xs[sl] = slab(sl);
 #pragma unroll
                 for (int t = 0; t < NT; ++t)
-                    p[t] = mma16<FMT_F16>(xs, q4_word_f16(u.w[t][sl / 4][sl % 4]), f4_t{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
-                for (int t = 0; t < NT; ++t) {
-                    if (sl > 0) {
-                        acc[t] += psc[t] * pend[t];
-                        __asm__ volatile("" : "+v"(acc[t]));
-                    }
-                    float sc = f16_bits_to_f32((uint16_t)(u.s[t][sl / 2] >> (16 * (sl % 2))));
-                    if constexpr (!SCALE16) {
-                        const int64_t b = e0 / 32 + sl;
-                        sc = b >= e1 / 32 && b < nc ? sc : 0.f;
-                    }
-                    pend[t] = p[t];
-                    psc[t] = sc;
-                }
-                __builtin_amdgcn_sched_barrier(0);               /* two slabs' values live at a time */
-            }
+                    for (int jj = 0; jj < J; ++jj) acc[t] = mma16<FMT>(xs[jj], u.w[t][jj], acc[t]);
+            } else if constexpr (FMT == FMT_I8) {
+                u32x4 xs[SL];
 #pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                acc[t] += psc[t] * pend[t];
-                __asm__ volatile("" : "+v"(acc[t]));
-            }
-        } else {                                                 /* 16-bit and int8: activations in registers */
-        if (__builtin_expect(SHORT || e0 < e1, 0)) {             /* a moved-back or short last step */
-            __asm__ volatile("" ::: "memory");                   /* kept a branch, not selects run every step */
-#pragma unroll
-            for (int s = 0; s < SL; ++s) {
-                const int64_t e = e0 + (XG * g + mma_x_byte<FMT>(s)) / 2;
-                u.x[s] = keep_if(e >= e1 && e < kelem, u.x[s]);
-            }
-            if constexpr (FMT != FMT_I8) {                       /* 16-bit weights there may not be finite */
+                for (int sl = 0; sl < SL; ++sl) xs[sl] = x8_i8_order(slab(sl));
 #pragma unroll
                 for (int t = 0; t < NT; ++t)
 #pragma unroll
                     for (int jj = 0; jj < J; ++jj) {
-                        const int64_t e = e0 + 32 * jj + 8 * g;
-                        u.w[t][jj] = keep_if(e >= e1 && e < kelem, u.w[t][jj]);
+                        acc[t] = mma16<FMT_F16>(xs[2 * jj], i8_words_f16(u.w[t][jj].x, u.w[t][jj].y), acc[t]);
+                        acc[t] = mma16<FMT_F16>(xs[2 * jj + 1], i8_words_f16(u.w[t][jj].z, u.w[t][jj].w), acc[t]);
                     }
-            }
-        }
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            if constexpr (FMT == FMT_I8) {
-#pragma unroll
-                for (int jj = 0; jj < J; ++jj) {
-                    acc[t] = mma16<FMT_F16>(x8_i8_order(u.x[2 * jj]), i8_words_f16(u.w[t][jj].x, u.w[t][jj].y), acc[t]);
-                    acc[t] = mma16<FMT_F16>(x8_i8_order(u.x[2 * jj + 1]), i8_words_f16(u.w[t][jj].z, u.w[t][jj].w), acc[t]);
-                }
             } else {
+                /* Each slab's products are scaled and summed while the next slab's matrix instructions
+                   run, and the sum is pinned there: left alone, the compiler sinks every scaled sum to
+                   the end of the unit and keeps all 32 products live (128 registers, one wave per SIMD
+                   instead of two). */
+                f4_t pend[NT];
+                float psc[NT];
 #pragma unroll
-                for (int jj = 0; jj < J; ++jj) acc[t] = mma16<FMT>(u.x[jj], u.w[t][jj], acc[t]);
+                for (int sl = 0; sl < SL; ++sl) {                   /* slab sl: block e0 / 32 + sl of each row */
+                    const u32x4 xs = x8_q4_order(slab(sl));
+                    f4_t p[NT];
+#pragma unroll
+                    for (int t = 0; t < NT; ++t)
+                        p[t] = mma16<FMT_F16>(xs, q4_word_f16(u.w[t][sl / 4][sl % 4]), f4_t{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) {
+                        if (sl > 0) {
+                            acc[t] += psc[t] * pend[t];
+                            __asm__ volatile("" : "+v"(acc[t]));
+                        }
+                        float sc = f16_bits_to_f32((uint16_t)(u.s[t][sl / 2] >> (16 * (sl % 2))));
+                        if constexpr (!SCALE16) {
+                            const int64_t b = e0 / 32 + sl;
+                            sc = b >= e1 / 32 && b < nc ? sc : 0.f;
+                        }
+                        pend[t] = p[t];
+                        psc[t] = sc;
+                    }
+                    __builtin_amdgcn_sched_barrier(0);               /* two slabs' values live at a time */
+                }
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    acc[t] += psc[t] * pend[t];
+                    __asm__ volatile("" : "+v"(acc[t]));
+                }
             }
-        }
         }
         if (kc + 1 == steps) {                                   /* end of a group: store, reset */
             /* lane (c, g) holds tokens 4 g .. 4 g + 3 of row c of each tile */

@@ -39,8 +39,11 @@ __global__ __launch_bounds__(WAVE) void k_sweep_mma(const DevMat* __restrict__ t
     const int64_t hi = base + q * (k + 1) + (int64_t)((uint64_t)r * (uint64_t)(k + 1) / nw);
     int hint = 0;
     if (lo >= hi) return;
-    /* the q4 ring: two units of 8 activation slabs and the scales, 64 16-byte chunks each (18 KiB) */
-    __shared__ u32x4 xlds[2 * MMA_LDS_SLOTS * WAVE];
+    /* the LDS ring: two units of the format's slots of 64 16-byte chunks (q4 18 KiB, int8 8 KiB,
+       16-bit 4 KiB; the kernel for mixed tables holds the largest) */
+    constexpr int F = mma_base_fmt(FMT);
+    constexpr int RING = F == 0 ? mma_ring_slots<FMT_Q4>() : mma_ring_slots<F>();
+    __shared__ u32x4 xlds[2 * RING * WAVE];
     if (main)
         stream_range_mma<FMT, MMA_TILES>(tab, cost, nmat, lo, hi, 0, 16 * MMA_TILES, token0, ntok, lane, hint, xlds);
     else
