@@ -705,11 +705,16 @@ extern "C" wsr_status wsr_decode_sweep_mma(const wsr_mat* mats, int32_t n, int32
     hipError_t e = hipSuccess;
     if (upload && (e = wsr::launch_put_table(dtab, dcost, p.tab.data(), n, ctr, s)) != hipSuccess)
         return hip_fail(e, "decode_sweep_mma: table upload");
-    std::vector<int64_t> max_group(p.segs.size(), 0), max_tail(p.segs.size(), 0);
+    /* per segment: the largest row group of 64 and of 128 rows, of the tail's rows, and the longest row */
+    std::vector<int64_t> max_g4(p.segs.size(), 0), max_g8(p.segs.size(), 0), max_tail(p.segs.size(), 0),
+        max_row(p.segs.size(), 0);
     for (size_t i = 0; i < p.segs.size(); ++i)
         for (int m = p.segs[i].first; m < p.segs[i].first + p.segs[i].count; ++m) {
-            max_group[i] = std::max(max_group[i], p.tab[m].row_bytes * std::min(p.tab[m].M, wsr::mma_group_rows()));
-            max_tail[i] = std::max(max_tail[i], p.tab[m].row_bytes * std::min(p.tab[m].M, wsr::mma_tail_rows()));
+            const int64_t rb = p.tab[m].row_bytes, M = p.tab[m].M;
+            max_g4[i] = std::max(max_g4[i], rb * std::min<int64_t>(M, 64));
+            max_g8[i] = std::max(max_g8[i], rb * std::min<int64_t>(M, 128));
+            max_tail[i] = std::max(max_tail[i], rb * std::min(M, wsr::mma_tail_rows()));
+            max_row[i] = std::max(max_row[i], p.tab[m].nc * 16);
         }
     std::vector<int> mma_fmt(p.segs.size());
     for (size_t i = 0; i < p.segs.size(); ++i) {
@@ -725,10 +730,12 @@ extern "C" wsr_status wsr_decode_sweep_mma(const wsr_mat* mats, int32_t n, int32
             const Seg& g = p.segs[i];
             /* a pass of one token would fill 16 token slots of every matrix instruction for one; the
                vector-ALU loop serves it instead (8B q4: 1.6k tok/s against 1.0k) */
+            const int tiles = wsr::mma_tiles(mma_fmt[i], ntok, max_row[i]);
             e = ntok == 1 ? wsr::launch_sweep(dtab + g.first, dcost + g.first, p.tab.data() + g.first, g.count, g.total,
                                               g.fmt, t, 1, ctr, s)
-                          : wsr::launch_sweep_mma(dtab + g.first, dcost + g.first, g.count, g.total, max_group[i],
-                                                  max_tail[i], mma_fmt[i], t, ntok, s);
+                          : wsr::launch_sweep_mma(dtab + g.first, dcost + g.first, g.count, g.total, tiles,
+                                                  tiles == 8 ? max_g8[i] : max_g4[i], max_tail[i], mma_fmt[i], t,
+                                                  ntok, s);
             if (e != hipSuccess) return hip_fail(e, "decode_sweep_mma: launch");
         }
     }

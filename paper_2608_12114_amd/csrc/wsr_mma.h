@@ -183,12 +183,17 @@ __device__ __forceinline__ const char* uniform_ptr(const char* p) {
    memory into a two-unit ring in the wave's LDS and are read back slab by slab as they are
    multiplied (8B q4 at 16 tokens 13.7k -> 14.1k tok/s, int8 protocol 74.7k -> 80.8k, 70B bf16
    +0.5 to +0.9 %).  Where a step's eight q4 block scales of a row are one aligned 16-byte run
-   (SCALE16), the unit's scales take one more slot of the ring: one load of 64 lanes brings the 16
-   bytes of each of the group's 64 rows, where loading them into registers took one instruction
-   per tile, each returning the same 16 bytes to all four lane groups.  mma_ring_slots is the
-   ring's slots of 64 chunks of 16 bytes per unit (0: no ring). */
-template <int FMT>
-constexpr int mma_ring_slots() { return FMT == FMT_Q4 ? MmaStep<FMT_Q4>::SLABS + 1 : MmaStep<FMT>::SLABS; }
+   (SCALE16), the unit's scales take more slots of the ring: each load of 64 lanes brings the 16
+   bytes of each of 64 rows of the group (one slot per 64 rows), where loading them into
+   registers took one instruction per tile, each returning the same 16 bytes to all four lane
+   groups.  mma_scale_slots and mma_ring_slots count slots of 64 chunks of 16 bytes per unit, for
+   row groups of NT tiles. */
+template <int NT>
+constexpr int mma_scale_slots() { return (16 * NT + WAVE - 1) / WAVE; }
+template <int FMT, int NT>
+constexpr int mma_ring_slots() {
+    return FMT == FMT_Q4 ? MmaStep<FMT_Q4>::SLABS + mma_scale_slots<NT>() : MmaStep<FMT>::SLABS;
+}
 
 /* Wait until at most n vector memory operations are outstanding (an LDS-DMA load's data is in LDS
    once it has left the count; operations leave it in the order they were issued). */
@@ -236,7 +241,9 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
     int lbuf = 0, mbuf = 0;                                      /* LDS ring half of the next load, multiply */
     rsrc_t rw = buffer_of(d.w), rs = buffer_of(d.w);             /* this group's row r0 of codes, scales */
     uint32_t vr[NT], vs[NT];                                     /* lane offsets: row of each tile */
-    uint32_t vsd = 0;                                            /* the row of lane i % 16 NT (scales to LDS) */
+    constexpr bool S_LDS = FMT == FMT_Q4 && SCALE16;
+    constexpr int NSD = S_LDS ? mma_scale_slots<NT>() : 0;      /* scale loads into LDS per unit */
+    uint32_t vsd[NSD > 0 ? NSD : 1] = {};                        /* row 64 j + i % 16 NT of lane i, load j */
     /* Ring activations reach LDS as whole 128-byte lines: load q of a unit (line p = q / 2 of the
        step, token half h = q % 2) gives lane i token 8 h + i / 8 at chunk (i % 8) ^ (i / 8) of line
        p, which holds slabs 2 p and 2 p + 1 (q4: chunk 4 (s % 2) + g of slab s for lane group g;
@@ -252,9 +259,8 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
 #pragma unroll
     for (int e = 0; e < 2; ++e)
         rd[e] = (c >> 3) * WAVE + (c & 7) * 8 + ((FMT == FMT_I8 ? e + 2 * g : 4 * e + g) ^ (c & 7));
-    constexpr bool S_LDS = FMT == FMT_Q4 && SCALE16;
-    constexpr int NDMA = SL + (S_LDS ? 1 : 0);                   /* loads into LDS per unit */
-    static_assert(NDMA <= mma_ring_slots<FMT>(), "LDS ring slots");
+    constexpr int NDMA = SL + NSD;                               /* loads into LDS per unit */
+    static_assert(NDMA <= mma_ring_slots<FMT, NT>(), "LDS ring slots");
     uint32_t vh[NT];                                             /* the row of the tile's second half */
     const uint32_t lc = 16 * (g + 4 * (c >> 3));                 /* the lane's byte within a 128-byte line */
     static_assert(J == 2, "a step is one line of each row");
@@ -271,7 +277,9 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
                 vr[t] = (uint32_t)((std::min<int64_t>(i0 + 16 * t + (c & 7), r1 - 1) - i0) * crb);
                 vh[t] = (uint32_t)((std::min<int64_t>(i0 + 16 * t + 8 + (c & 7), r1 - 1) - i0) * crb);
             }
-            if constexpr (S_LDS) vsd = (uint32_t)((std::min<int64_t>(i0 + lane % (16 * NT), r1 - 1) - i0) * srow);
+#pragma unroll
+            for (int j = 0; j < NSD; ++j)
+                vsd[j] = (uint32_t)((std::min<int64_t>(i0 + (WAVE * j + lane) % (16 * NT), r1 - 1) - i0) * srow);
         }
         /* the last step ends at the row's end; offsets stay below 2^31 (the caller's limits) */
         const uint32_t kb = SHORT ? 0 : (uint32_t)std::min<int64_t>((int64_t)kl * SB, crb - SB);
@@ -288,7 +296,8 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
                                          : xt[h] + 16 * xc + 128 * p;
                 buf_to_lds(rx, ring + q * WAVE, v, xo);
             }
-            if constexpr (S_LDS) buf_to_lds(rs, ring + SL * WAVE, vsd, b0 * 2);
+#pragma unroll
+            for (int j = 0; j < NSD; ++j) buf_to_lds(rs, ring + (SL + j) * WAVE, vsd[j], b0 * 2);
             lbuf ^= 1;
             __builtin_amdgcn_sched_barrier(0);
         }

@@ -14,13 +14,16 @@ namespace wsr {
    the kernel with every q4 loop). */
 constexpr int FMT_Q4_WHOLE = 8;
 
-/* Tokens token0 .. token0 + ntok - 1 (ntok <= 16) of the sweep on the matrix cores; max_group and
-   max_tail_group are the largest row group's weight-stream bytes (mma_group_rows() rows, and
-   mma_tail_rows() rows for the tail of the stream, of any matrix in the table). */
-int64_t mma_group_rows();
+/* Tokens token0 .. token0 + ntok - 1 (ntok <= 16) of the sweep on the matrix cores, in row groups
+   of 16 tiles rows (tiles 4 or 8, as mma_tiles chooses for the table's format, the pass's tokens
+   and its longest row); max_group and max_tail_group are the largest row group's weight-stream
+   bytes (16 tiles rows, and mma_tail_rows() rows for the tail of the stream, of any matrix in the
+   table). */
+int mma_tiles(int fmt_all, int ntok, int64_t max_row_bytes);
 int64_t mma_tail_rows();
-hipError_t launch_sweep_mma(const DevMat* tab, const int64_t* cost, int nmat, int64_t total, int64_t max_group,
-                            int64_t max_tail_group, int fmt_all, int32_t token0, int ntok, hipStream_t s);
+hipError_t launch_sweep_mma(const DevMat* tab, const int64_t* cost, int nmat, int64_t total, int tiles,
+                            int64_t max_group, int64_t max_tail_group, int fmt_all, int32_t token0, int ntok,
+                            hipStream_t s);
 
 }  // namespace wsr
 

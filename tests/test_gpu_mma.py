@@ -82,6 +82,25 @@ def test_mma_matrix_parity_and_bounds(fmt, T):
         assert rel_l2(y[t, :M], want) <= TOL, (fmt, t)
 
 
+# groups of 128 rows (eight tiles: 16-bit at any token count, q4 from 8 tokens, int8 from 12) over
+# several whole groups and a ragged last one, against four tiles where the token count picks them
+GROUPS128 = [(wl.BF16, 300, 1000), (wl.F16, 129, 512), (wl.Q4, 300, 2048), (wl.Q4, 260, 2080), (wl.I8, 300, 1024)]
+
+
+@pytest.mark.parametrize("fmt,M,K", GROUPS128, ids=lambda v: str(v))
+@pytest.mark.parametrize("T", [2, 8, 12, 16])
+def test_mma_row_groups_parity_and_bounds(fmt, M, K, T):
+    W, S = host_matrix(fmt, M, K, seed=13)
+    xfmt = wl.BF16 if fmt == wl.BF16 else wl.F16
+    X = synth.normal16((T + 1, K), wl.X_SIGMA, xfmt, seed=13, stream=607)
+    y = run_mma(fmt, W, S, X, M, K, T, y_rows=M + 3)
+    assert np.isnan(y[:, M:]).all() and np.isnan(y[T:]).all()
+    ora = oracle.get()
+    for t in range(T):
+        want = ora.gemv(dict(fmt=fmt, w=W, s=S), X[t]) if fmt in (wl.Q4, wl.I8) else ora.gemv16(W, X[t], fmt)
+        assert rel_l2(y[t, :M], want) <= TOL, (fmt, t)
+
+
 def sweep_pair(inp, tokens, chained=False):
     """(vector-ALU sweep outputs, matrix-core sweep outputs) for the same inputs."""
     mats = wsr.make_mats(inp.specs(chained=chained))
