@@ -183,17 +183,18 @@ __device__ __forceinline__ const char* uniform_ptr(const char* p) {
    memory into a two-unit ring in the wave's LDS and are read back slab by slab as they are
    multiplied (8B q4 at 16 tokens 13.7k -> 14.1k tok/s, int8 protocol 74.7k -> 80.8k, 70B bf16
    +0.5 to +0.9 %).  Where a step's eight q4 block scales of a row are one aligned 16-byte run
-   (SCALE16), the unit's scales take more slots of the ring: each load of 64 lanes brings the 16
-   bytes of each of 64 rows of the group (one slot per 64 rows), where loading them into
-   registers took one instruction per tile, each returning the same 16 bytes to all four lane
-   groups.  mma_scale_slots and mma_ring_slots count slots of 64 chunks of 16 bytes per unit, for
-   row groups of NT tiles. */
-template <int NT>
-constexpr int mma_scale_slots() { return (16 * NT + WAVE - 1) / WAVE; }
+   (SCALE16), the scales of MMA_SCALE_STEPS steps of the group's rows come into LDS at once, one
+   load of 64 lanes per 16 rows (64 contiguous bytes of each row), where loading a step's scales
+   into registers took one instruction per tile, each returning the same 16 bytes of a row to all
+   four lane groups, and touched a cache line per row per step (8B q4 at 16 tokens: 15.7k ->
+   17.8k tok/s; at 4 tokens 4.4k -> 4.9k).  mma_ring_slots counts the ring's slots of 64 chunks of 16 bytes: the two units'
+   activations, then (q4) one block of scales for row groups of NT tiles. */
+constexpr int MMA_SCALE_STEPS = 4;
 template <int FMT, int NT>
-constexpr int mma_ring_slots() {
-    return FMT == FMT_Q4 ? MmaStep<FMT_Q4>::SLABS + mma_scale_slots<NT>() : MmaStep<FMT>::SLABS;
-}
+constexpr int mma_ring_slots() { return 2 * MmaStep<FMT>::SLABS + (FMT == FMT_Q4 ? NT : 0); }
+
+/* Wait until no LDS operation of the wave is outstanding. */
+__device__ __forceinline__ void wait_lds_idle() { __builtin_amdgcn_s_waitcnt(0xF | 0x70 | (3 << 14)); }
 
 /* Wait until at most n vector memory operations are outstanding (an LDS-DMA load's data is in LDS
    once it has left the count; operations leave it in the order they were issued). */
@@ -241,9 +242,18 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
     int lbuf = 0, mbuf = 0;                                      /* LDS ring half of the next load, multiply */
     rsrc_t rw = buffer_of(d.w), rs = buffer_of(d.w);             /* this group's row r0 of codes, scales */
     uint32_t vr[NT], vs[NT];                                     /* lane offsets: row of each tile */
+    /* q4 SCALE16: the block of scales of steps 4 m .. 4 m + 3 of the group's 16 NT rows comes into
+       LDS with the first of those steps, NT loads of 16 rows each: lane i of load j brings row
+       r = 16 j + i / 4 at step 4 m + ((i % 4) ^ (r / 2 % 4)), into block slot 4 r + i % 4 (the
+       rotation spreads a tile's 16 rows of one step over the LDS banks).  The block is overwritten
+       when the next one comes, one unit before the old block's last unit is multiplied, so that
+       unit's scales are read into its registers at the end of the unit before it (scar). */
     constexpr bool S_LDS = FMT == FMT_Q4 && SCALE16;
-    constexpr int NSD = S_LDS ? mma_scale_slots<NT>() : 0;      /* scale loads into LDS per unit */
-    uint32_t vsd[NSD > 0 ? NSD : 1] = {};                        /* row 64 j + i % 16 NT of lane i, load j */
+    constexpr int NBD = S_LDS ? NT : 0;                          /* loads of a scale block */
+    constexpr int SBLK = 2 * SL * WAVE;                          /* the block's first slot */
+    uint32_t vsb[NBD > 0 ? NBD : 1] = {};                        /* row 16 j + i / 4 of lane i, load j */
+    const uint32_t skk = (uint32_t)((lane & 3) ^ ((lane >> 3) & 3));   /* its step within the block */
+    bool scar = false;                                           /* the next unit's scales are in its registers */
     /* Ring activations reach LDS as whole 128-byte lines: load q of a unit (line p = q / 2 of the
        step, token half h = q % 2) gives lane i token 8 h + i / 8 at chunk (i % 8) ^ (i / 8) of line
        p, which holds slabs 2 p and 2 p + 1 (q4: chunk 4 (s % 2) + g of slab s for lane group g;
@@ -259,11 +269,20 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
 #pragma unroll
     for (int e = 0; e < 2; ++e)
         rd[e] = (c >> 3) * WAVE + (c & 7) * 8 + ((FMT == FMT_I8 ? e + 2 * g : 4 * e + g) ^ (c & 7));
-    constexpr int NDMA = SL + NSD;                               /* loads into LDS per unit */
-    static_assert(NDMA <= mma_ring_slots<FMT, NT>(), "LDS ring slots");
+    static_assert(2 * SL + NBD <= mma_ring_slots<FMT, NT>(), "LDS ring slots");
     uint32_t vh[NT];                                             /* the row of the tile's second half */
     const uint32_t lc = 16 * (g + 4 * (c >> 3));                 /* the lane's byte within a 128-byte line */
     static_assert(J == 2, "a step is one line of each row");
+    /* the scales of step k of tile t's row c (lane (c, g)) from the block */
+    auto read_scales = [&](Unit& v, int32_t k) {
+        if constexpr (S_LDS) {
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const u32x4 x = xlds[SBLK + 4 * (16 * t + c) + ((k % MMA_SCALE_STEPS) ^ ((c >> 1) & 3))];
+                v.s[t][0] = x.x, v.s[t][1] = x.y, v.s[t][2] = x.z, v.s[t][3] = x.w;
+            }
+        }
+    };
     auto load = [&](Unit& u) {
         if (kl == 0) {
             const int64_t i0 = r0 + gl * 16 * NT;
@@ -278,17 +297,23 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
                 vh[t] = (uint32_t)((std::min<int64_t>(i0 + 16 * t + 8 + (c & 7), r1 - 1) - i0) * crb);
             }
 #pragma unroll
-            for (int j = 0; j < NSD; ++j)
-                vsd[j] = (uint32_t)((std::min<int64_t>(i0 + (WAVE * j + lane) % (16 * NT), r1 - 1) - i0) * srow);
+            for (int j = 0; j < NBD; ++j)
+                vsb[j] = (uint32_t)((std::min<int64_t>(i0 + 16 * j + (lane >> 2), r1 - 1) - i0) * srow);
         }
         /* the last step ends at the row's end; offsets stay below 2^31 (the caller's limits) */
         const uint32_t kb = SHORT ? 0 : (uint32_t)std::min<int64_t>((int64_t)kl * SB, crb - SB);
         const uint32_t xo = SHORT ? 0 : (uint32_t)(std::min<int64_t>((int64_t)kl * SK, kelem - SK) * 2);
         const uint32_t b0 = SHORT ? 0 : (uint32_t)std::min<int64_t>((int64_t)kl * 8, nc - 8);   /* q4: first block */
+        if (S_LDS && kl % MMA_SCALE_STEPS == 0) {              /* a new block of scales, first of all */
+            wait_lds_idle();                                     /* the old block's reads are done */
+            const uint32_t so = (uint32_t)std::min<int64_t>(kl + skk, steps - 1) * 16;   /* the last block may be short */
+#pragma unroll
+            for (int j = 0; j < NBD; ++j) buf_to_lds(rs, xlds + SBLK + j * WAVE, vsb[j] + so, 0);
+        }
         {
-            /* the slabs (and scales) first, so that every load issued after them is counted by
-               wait_vm; a row shorter than one step clamps each lane's activation offset */
-            u32x4* ring = xlds + (lbuf ? NDMA * WAVE : 0);
+            /* the slabs next, so that every load issued after them is counted by wait_vm; a row
+               shorter than one step clamps each lane's activation offset */
+            u32x4* ring = xlds + (lbuf ? SL * WAVE : 0);
 #pragma unroll
             for (int q = 0; q < SL; ++q) {
                 const int p = q >> 1, h = q & 1;
@@ -296,8 +321,6 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
                                          : xt[h] + 16 * xc + 128 * p;
                 buf_to_lds(rx, ring + q * WAVE, v, xo);
             }
-#pragma unroll
-            for (int j = 0; j < NSD; ++j) buf_to_lds(rs, ring + (SL + j) * WAVE, vsd[j], b0 * 2);
             lbuf ^= 1;
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -327,9 +350,11 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
        int8 row scales, loaded on a group's last step only, are left out: a wait that counts fewer
        later loads than were issued still covers the ring). */
     constexpr int AFTER_X = NT * J + (FMT == FMT_Q4 ? (SCALE16 ? 0 : 8 * NT) : 0);
-    constexpr int PER_UNIT = NDMA + AFTER_X;
-    auto multiply = [&](Unit& u, auto next_loaded) {
+    constexpr int PER_UNIT = SL + AFTER_X;                       /* plus NBD where a scale block starts */
+    auto multiply = [&](Unit& u, Unit& un, auto next_loaded) {   /* un: the next unit's registers */
         const int64_t i0 = r0 + gc * 16 * NT;
+        const int32_t k1 = kc + 1 == steps ? 0 : kc + 1;         /* the next unit's step, and the one after */
+        const int32_t k2 = k1 + 1 == steps ? 0 : k1 + 1;
         /* the step's first weight, and the first one it has not already covered */
         const int64_t e0 = SHORT ? 0 : std::min<int64_t>((int64_t)kc * SK, kelem - SK), e1 = SHORT ? 0 : (int64_t)kc * SK;
 #pragma unroll
@@ -341,18 +366,18 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
 #pragma unroll
                     for (int jj = 0; jj < J; ++jj) u.w[t][jj] = transpose_groups(u.w[t][jj]);
             }
-            /* the unit's slabs are in LDS once no more than the loads issued after them remain */
+            /* the unit's slabs are in LDS once no more than the loads issued after them remain (the
+               next unit's scale block, if it starts one, was issued after them too) */
             constexpr int AFTER = AFTER_X + (decltype(next_loaded)::value ? PER_UNIT : 0);
-            wait_vm<(AFTER < 63 ? AFTER : 63)>();
+            if (S_LDS && decltype(next_loaded)::value && k1 % MMA_SCALE_STEPS == 0)
+                wait_vm<(AFTER + NBD < 63 ? AFTER + NBD : 63)>();
+            else
+                wait_vm<(AFTER < 63 ? AFTER : 63)>();
             __builtin_amdgcn_sched_barrier(0);
-            const u32x4* ring = xlds + (mbuf ? NDMA * WAVE : 0);
+            const u32x4* ring = xlds + (mbuf ? SL * WAVE : 0);
             mbuf ^= 1;
-            if constexpr (S_LDS) {                               /* lane (c, g): row c of each tile */
-#pragma unroll
-                for (int t = 0; t < NT; ++t) {
-                    const u32x4 v = ring[SL * WAVE + 16 * t + c];
-                    u.s[t][0] = v.x, u.s[t][1] = v.y, u.s[t][2] = v.z, u.s[t][3] = v.w;
-                }
+            if constexpr (S_LDS) {
+                if (!scar) read_scales(u, kc);
             }
             const bool masked = SHORT || e0 < e1;                /* a short row or a moved-back last step */
             auto slab = [&](int sl) -> u32x4 {
@@ -427,6 +452,15 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
                     __asm__ volatile("" : "+v"(acc[t]));
                 }
             }
+            /* The next unit's scales, where the unit after it brings a new block before the next
+               unit is multiplied; a block of one step (the group's last) is waited for first. */
+            if constexpr (S_LDS && decltype(next_loaded)::value) {
+                scar = k2 % MMA_SCALE_STEPS == 0;
+                if (scar) {
+                    if (k1 % MMA_SCALE_STEPS == 0) wait_vm<(SL + NT * J < 63 ? SL + NT * J : 63)>();
+                    read_scales(un, k1);
+                }
+            }
         }
         if (kc + 1 == steps) {                                   /* end of a group: store, reset */
             /* lane (c, g) holds tokens 4 g .. 4 g + 3 of row c of each tile */
@@ -453,23 +487,30 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
     const std::true_type next_loaded;
     const std::false_type last;
     load(buf[0]);
+    if constexpr (S_LDS) {                                       /* one-step groups: unit 1 brings a new block */
+        if (steps == 1 && n > 1) {
+            wait_vm<(SL + NT * J < 63 ? SL + NT * J : 63)>();
+            read_scales(buf[0], 0);
+            scar = true;
+        }
+    }
     int64_t u = 0;                                               /* buf[0] holds unit u */
     for (; u + 3 <= n; u += 2) {
         load(buf[1]);                                            /* unit u + 1 */
         __builtin_amdgcn_sched_barrier(0);
-        multiply(buf[0], next_loaded);                           /* unit u     */
+        multiply(buf[0], buf[1], next_loaded);                   /* unit u     */
         load(buf[0]);                                            /* unit u + 2 */
         __builtin_amdgcn_sched_barrier(0);
-        multiply(buf[1], next_loaded);                           /* unit u + 1 */
+        multiply(buf[1], buf[0], next_loaded);                   /* unit u + 1 */
     }
     /* one or two units left, unit u in buf[0] */
     if (u + 1 < n) {
         load(buf[1]);
         __builtin_amdgcn_sched_barrier(0);
-        multiply(buf[0], next_loaded);
-        multiply(buf[1], last);
+        multiply(buf[0], buf[1], next_loaded);
+        multiply(buf[1], buf[0], last);
     } else {
-        multiply(buf[0], last);
+        multiply(buf[0], buf[1], last);
     }
 }
 

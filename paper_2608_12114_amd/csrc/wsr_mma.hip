@@ -25,7 +25,8 @@ constexpr int64_t SWEEP_SPAN_MMA = 64 << 10;  /* least bytes of the weight strea
    quarter of a group's work.  A matrix's rows from the first main-group boundary at or after byte
    `tail` on belong to the tail, the rows before it to the main spans. */
 template <int FMT, int NT>
-__global__ __launch_bounds__(WAVE) void k_sweep_mma(const DevMat* __restrict__ tab, const int64_t* __restrict__ cost,
+__global__ __launch_bounds__(WAVE) __attribute__((amdgpu_waves_per_eu(FMT == FMT_Q4_WHOLE ? 2 : 1)))
+void k_sweep_mma(const DevMat* __restrict__ tab, const int64_t* __restrict__ cost,
                                                     int nmat, int64_t total, int64_t tail, int64_t w1,
                                                     int32_t token0, int ntok) {
     const int lane = threadIdx.x;
@@ -38,12 +39,12 @@ __global__ __launch_bounds__(WAVE) void k_sweep_mma(const DevMat* __restrict__ t
     const int64_t hi = base + q * (k + 1) + (int64_t)((uint64_t)r * (uint64_t)(k + 1) / nw);
     int hint = 0;
     if (lo >= hi) return;
-    /* the LDS ring: two units of the format's slots of 64 16-byte chunks (at four tiles q4 18 KiB,
-       int8 8 KiB, 16-bit 4 KiB; the kernel for mixed tables holds the largest); the tail's
-       one-tile groups need no more */
+    /* the LDS ring: slots of 64 16-byte chunks (at four tiles q4 20 KiB, int8 8 KiB, 16-bit
+       4 KiB; the kernel for mixed tables holds the largest); the tail's one-tile groups need no
+       more */
     constexpr int F = mma_base_fmt(FMT);
     constexpr int RING = F == 0 ? mma_ring_slots<FMT_Q4, NT>() : mma_ring_slots<F, NT>();
-    __shared__ u32x4 xlds[2 * RING * WAVE];
+    __shared__ u32x4 xlds[RING * WAVE];
     if (main)
         stream_range_mma<FMT, NT>(tab, cost, nmat, lo, hi, 0, 16 * NT, token0, ntok, lane, hint, xlds);
     else
