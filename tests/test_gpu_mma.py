@@ -101,6 +101,22 @@ def test_mma_row_groups_parity_and_bounds(fmt, M, K, T):
         assert rel_l2(y[t, :M], want) <= TOL, (fmt, t)
 
 
+# q4 rows of a whole number of 8-block steps take their scales in blocks of four steps; rows of 1,
+# 2, 3, 5, 6 and 7 steps end in a partial block (one step: every group's only unit carries its
+# scales across the next group's block), over several row groups with a ragged last one
+@pytest.mark.parametrize("K", [256, 512, 768, 1280, 1536, 1792])
+@pytest.mark.parametrize("T", [3, 16])
+def test_mma_q4_scale_blocks(K, T):
+    M = 150
+    W, S = host_matrix(wl.Q4, M, K, seed=14)
+    X = synth.normal16((T + 1, K), wl.X_SIGMA, wl.F16, seed=14, stream=608)
+    y = run_mma(wl.Q4, W, S, X, M, K, T, y_rows=M + 3)
+    assert np.isnan(y[:, M:]).all() and np.isnan(y[T:]).all()
+    ora = oracle.get()
+    for t in range(T):
+        assert rel_l2(y[t, :M], ora.gemv(dict(fmt=wl.Q4, w=W, s=S), X[t])) <= TOL, (K, t)
+
+
 def sweep_pair(inp, tokens, chained=False):
     """(vector-ALU sweep outputs, matrix-core sweep outputs) for the same inputs."""
     mats = wsr.make_mats(inp.specs(chained=chained))
