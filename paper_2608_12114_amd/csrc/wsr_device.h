@@ -46,6 +46,40 @@ __device__ __forceinline__ u32x4 load_reused(g_u32x4* p) { return *p; }
 __device__ __forceinline__ u32x4 zero4() { return u32x4{0u, 0u, 0u, 0u}; }
 
 /* The wave's index inside its block, as a uniform (scalar) value. */
+/* Raw buffer access: a wave-uniform base in a scalar resource, a 32-bit lane offset, a scalar
+   offset and an immediate, with no per-lane address arithmetic.  Every access here is in bounds
+   by construction, so the resource's range check is left open (num_records = 2^32 - 1); the word
+   0x00020000 is the gfx9 family's format for untyped buffer access.  aux 2 marks a load
+   non-temporal (read once). */
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+__device__ __forceinline__ rsrc_t buffer_of(const void* base) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, -1, 0x00020000);
+}
+__device__ __forceinline__ u32x4 buf_once(rsrc_t r, uint32_t v, uint32_t s) {
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, v, s, 2));
+}
+__device__ __forceinline__ u32x4 buf_reused(rsrc_t r, uint32_t v, uint32_t s) {
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, v, s, 0));
+}
+__device__ __forceinline__ uint32_t buf_u16(rsrc_t r, uint32_t v, uint32_t s) {
+    return __builtin_amdgcn_raw_buffer_load_b16(r, v, s, 0);
+}
+/* 16 bytes per lane from memory straight into LDS: lane i's bytes land at lds + 16 i (lds
+   wave-uniform).  The load counts in vmcnt like any other; nothing orders a later LDS read of the
+   same bytes after it except an explicit wait (wait_vm). */
+__device__ __forceinline__ void buf_to_lds(rsrc_t r, u32x4* lds, uint32_t v, uint32_t s) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, v, s, 0, 0);
+}
+
+/* A wave-uniform pointer held in scalar registers, so that a load from it plus a 32-bit lane
+   offset and a constant takes the scalar-base form (no per-lane address arithmetic). */
+__device__ __forceinline__ const char* uniform_ptr(const char* p) {
+    const uint64_t v = reinterpret_cast<uint64_t>(p);
+    const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return reinterpret_cast<const char*>(hi << 32 | lo);
+}
+
 __device__ __forceinline__ int wave_in_block() {
     return __builtin_amdgcn_readfirstlane((int)(threadIdx.x / WAVE));
 }
@@ -827,16 +861,33 @@ __device__ __forceinline__ void rows_q4(const DevMat& d, int64_t r0, int64_t r1,
         for (int r = 0; r < R; ++r) acc[r] = 0.f;
         int64_t gl = 0, kl = 0;                          /* next unit to load    */
         int64_t gc = 0, kc = 0;                          /* next unit to decode  */
+        /* Raw buffer loads: a resource per row group and a scalar offset per row and step (rows of a
+           group lie within 2^28 bytes) over one lane offset, where 64-bit row pointers cost several
+           scalar instructions per row and step (8B q4: 95 -> 25 scalar instructions per unit in the
+           main loop, the same 164 registers; the rate moved by under 0.3 %, the outputs not at all). */
+        const rsrc_t rx = buffer_of(uniform_ptr(static_cast<const char*>(d.x) + (int64_t)token * d.x_stride));
+        rsrc_t rw = rx, rsc = rx;                        /* this group's codes and scales */
+        const uint32_t vl = 16u * (uint32_t)lane, vx = 64u * (uint32_t)lane;
+        const uint32_t rcb = (uint32_t)(nb * 16), rsb = (uint32_t)(nb * 2);   /* row bytes of codes, scales */
         auto load = [&](Q4Step<R, U>& st) {
-            g_u32x4* wr[R];
-            g_u16* sr[R];
-            const int64_t i = r0 + gl * R;
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                wr[r] = Wq + (i + r) * nb;
-                sr[r] = S + (i + r) * nb;
+            if (kl == 0) {
+                const int64_t i = r0 + gl * R;
+                rw = buffer_of(uniform_ptr(static_cast<const char*>(d.w) + i * nb * 16));
+                rsc = buffer_of(uniform_ptr(static_cast<const char*>(d.s) + i * nb * 2));
             }
-            q4_load<R, U>(st, wr, sr, x, kl * STEP, lane);
+            const uint32_t kb = (uint32_t)(kl * STEP);   /* the step's first block */
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    st.x[u][j] = buf_reused(rx, vx + (uint32_t)(4096 * u + 16 * j), 64u * kb);
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    st.w[r][u] = buf_once(rw, vl + (uint32_t)(1024 * u), r * rcb + 16u * kb);
+                    st.s[r][u] = (uint16_t)buf_u16(rsc, (vl >> 3) + (uint32_t)(128 * u), r * rsb + 2u * kb);
+                }
             if (++kl == steps) { kl = 0; ++gl; }
         };
         auto decode = [&](const Q4Step<R, U>& st) {

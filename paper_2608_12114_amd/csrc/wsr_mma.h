@@ -148,37 +148,6 @@ constexpr int mma_x_byte(int s) { return FMT == FMT_I8 ? 128 * (s / 2) + 16 * (s
 
 __device__ __forceinline__ u32x4 keep_if(bool ok, u32x4 v) { return ok ? v : zero4(); }
 
-/* Raw buffer access: a wave-uniform base in a scalar resource, a 32-bit lane offset, a scalar
-   offset and an immediate, with no per-lane address arithmetic.  Every access here is in bounds
-   by construction, so the resource's range check is left open (num_records = 2^32 - 1); the word
-   0x00020000 is the gfx9 family's format for untyped buffer access.  aux 2 marks a load
-   non-temporal (read once). */
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-__device__ __forceinline__ rsrc_t buffer_of(const void* base) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, -1, 0x00020000);
-}
-__device__ __forceinline__ u32x4 buf_once(rsrc_t r, uint32_t v, uint32_t s) {
-    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, v, s, 2));
-}
-__device__ __forceinline__ uint32_t buf_u16(rsrc_t r, uint32_t v, uint32_t s) {
-    return __builtin_amdgcn_raw_buffer_load_b16(r, v, s, 0);
-}
-/* 16 bytes per lane from memory straight into LDS: lane i's bytes land at lds + 16 i (lds
-   wave-uniform).  The load counts in vmcnt like any other; nothing orders a later LDS read of the
-   same bytes after it except an explicit wait (wait_vm). */
-__device__ __forceinline__ void buf_to_lds(rsrc_t r, u32x4* lds, uint32_t v, uint32_t s) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, v, s, 0, 0);
-}
-
-/* A wave-uniform pointer held in scalar registers, so that a load from it plus a 32-bit lane
-   offset and a constant takes the scalar-base form (no per-lane address arithmetic). */
-__device__ __forceinline__ const char* uniform_ptr(const char* p) {
-    const uint64_t v = reinterpret_cast<uint64_t>(p);
-    const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
-    const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
-    return reinterpret_cast<const char*>(hi << 32 | lo);
-}
-
 /* The activations stay out of the register ring: each unit's activation slabs go straight from
    memory into a two-unit ring in the wave's LDS and are read back slab by slab as they are
    multiplied (8B q4 at 16 tokens 13.7k -> 14.1k tok/s, int8 protocol 74.7k -> 80.8k, 70B bf16
