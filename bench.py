@@ -564,6 +564,12 @@ def row_protocol(stream, wsr, warmup_passes=12, passes=31, tokens=16, want_cpu=T
     # launch latency that a pass bracketed by its own synchronisation includes
     for _ in range(warmup_passes):
         one()
+    t0 = time.perf_counter()                # untimed for at least 0.5 s, as the other rows are
+    while time.perf_counter() - t0 < 0.5:
+        for _ in range(8):
+            one()
+        torch.cuda.synchronize()
+    res["warmup_seconds_one_launch"] = round(time.perf_counter() - t0, 3)
     b2b = [timed(one, 8, stream) / 8 * 1e3 for _ in range(passes)]
     st = spread(b2b)
     res["one_launch_back_to_back"] = {"median_ms_per_pass": st["median"], "iqr_ms": st["iqr"],
