@@ -182,8 +182,9 @@ __device__ __forceinline__ void wait_vm() {
    is not a whole number of steps, its last step is moved back to end at the row's end and the
    values the previous step already covered are zeroed when it is multiplied (masking them as they
    arrive would make each load wait at once).  Rows shorter than one step (SHORT) clamp each
-   lane's offset instead.  q4 reads a step's eight block scales as one 16-byte load where the rows
-   hold a multiple of 8 blocks and the scales are 16-byte aligned (SCALE16); otherwise one by one.
+   lane's offset instead.  Where q4 rows hold a whole number of 8-block steps and the scales are
+   16-byte aligned (SCALE16), a step's eight block scales of a row are one 16-byte run and come
+   through LDS in blocks of four steps (below); otherwise each is loaded into registers alone.
    The caller keeps 16 NT rows of codes and 16 tokens of activations within 2^31 bytes.  The
    activations (and, with SCALE16, the q4 scales) come from the LDS ring, which leaves the register
    ring to the weights. */
