@@ -266,10 +266,10 @@ wsr_status wsr_decode_sweep_ordered(const wsr_mat* mats, int32_t n, int32_t n_to
    so the copy of chunk k + 1 overlaps the GEMV of chunk k.  The first copy waits for the work
    already enqueued on `stream`; on return, all work of the call is ordered before later work on
    `stream`.  Use distinct streams for overlap (the same stream also works, serially).  The source
-   memory must stay valid and unchanged until the copies have run.  A copy from pageable host
-   memory may run on the host as soon as it is issued, ahead of the stream's earlier waits; for such
-   sources the call therefore waits on the host, before each copy into a half, until the GEMV that
-   last read that half has run (the call blocks).  mats: as wsr_decode_sweep, except that w and scales may
+   memory must stay valid and unchanged until the copies have run.  Pageable host sources go
+   through two pinned host halves the library keeps per device (each the size of a stage half):
+   host threads copy a chunk into one half while the DMA engine moves the previous chunk out of
+   the other, so for such sources the call blocks until its last chunk is in a pinned half.  mats: as wsr_decode_sweep, except that w and scales may
    be host pointers; x and y device memory.  WSR_E_SIZE if half of stage_bytes, less 256, holds no
    row of some matrix.  Calls on one device are serialised while they enqueue (events shared per
    device). */

@@ -8,10 +8,13 @@
 #include <unistd.h>
 
 #include <algorithm>
+#include <condition_variable>
 #include <cstdarg>
 #include <cstdio>
+#include <cstring>
 #include <map>
 #include <mutex>
+#include <thread>
 #include <vector>
 
 #include "wsr.h"
@@ -533,9 +536,7 @@ hipError_t make_stage_events(StageEvents& e) {
     return hipSuccess;
 }
 
-/* True for host memory the runtime has not registered (pageable).  A copy from such memory may be
-   carried out on the host when it is issued, ahead of the waits already enqueued on its stream, so
-   the staged sweep orders those copies with host-side waits instead. */
+/* True for host memory the runtime has not registered (pageable). */
 bool pageable(const void* p) {
     if (!p) return false;
     hipPointerAttribute_t a{};
@@ -544,6 +545,112 @@ bool pageable(const void* p) {
         return true;
     }
     return a.type == hipMemoryTypeUnregistered;
+}
+
+/* Host threads for copies out of pageable memory: copy() splits a range into slices of at least
+   4 MiB over up to 8 threads (the calling thread takes one) and returns when all are done.  The
+   threads live for the process (detached, waiting on a condition variable). */
+class CopyPool {
+public:
+    static CopyPool& get() {
+        static CopyPool* p = new CopyPool();
+        return *p;
+    }
+    void copy(char* dst, const char* src, size_t n) {
+        std::lock_guard<std::mutex> one(call_mu_);      /* one range at a time */
+        constexpr size_t MIN_SLICE = 4u << 20;
+        const size_t parts = std::max<size_t>(1, std::min<size_t>(nthreads_ + 1, n / MIN_SLICE));
+        if (parts == 1) {
+            std::memcpy(dst, src, n);
+            return;
+        }
+        const size_t per = (n + parts - 1) / parts;
+        {
+            std::lock_guard<std::mutex> l(mu_);
+            jobs_.clear();
+            for (size_t i = 1; i < parts; ++i) {
+                const size_t a = i * per, b = std::min(n, a + per);
+                if (a < b) jobs_.push_back({dst + a, src + a, b - a});
+            }
+            next_ = 0;
+            left_ = jobs_.size();
+        }
+        cv_.notify_all();
+        std::memcpy(dst, src, std::min(n, per));
+        std::unique_lock<std::mutex> l(mu_);
+        done_.wait(l, [&] { return left_ == 0; });
+    }
+
+private:
+    struct Job {
+        char* d;
+        const char* s;
+        size_t n;
+    };
+    CopyPool() {
+        const unsigned hw = std::thread::hardware_concurrency();
+        nthreads_ = std::max(1u, std::min(8u, hw / 2));
+        for (unsigned i = 0; i < nthreads_; ++i) std::thread([this] { run(); }).detach();
+    }
+    void run() {
+        std::unique_lock<std::mutex> l(mu_);
+        for (;;) {
+            cv_.wait(l, [&] { return next_ < jobs_.size(); });
+            const Job j = jobs_[next_++];
+            l.unlock();
+            std::memcpy(j.d, j.s, j.n);
+            l.lock();
+            if (--left_ == 0) done_.notify_all();
+        }
+    }
+    std::mutex call_mu_, mu_;
+    std::condition_variable cv_, done_;
+    std::vector<Job> jobs_;
+    size_t next_ = 0, left_ = 0;
+    unsigned nthreads_ = 1;
+};
+
+/* Pinned host halves, per device, through which the staged sweep moves pageable sources: host
+   threads copy a chunk into one half while the DMA engine moves the previous chunk out of the
+   other.  A copy straight from pageable memory goes through the runtime's own staging (about
+   28 GB/s from a file's page-cache pages, against 57 GB/s for a pinned source).  Kept for the life
+   of the process; grown (after the halves' last copies have run) when a call needs more.  The
+   staged sweep's per-device mutex guards them. */
+struct Bounce {
+    char* half[2] = {nullptr, nullptr};
+    size_t bytes = 0;
+    hipEvent_t out[2]{};                                 /* the last copy out of each half */
+    bool pending[2] = {false, false};
+    bool made = false;
+};
+Bounce g_bounce[64];
+
+hipError_t bounce_ready(Bounce& b, size_t bytes) {
+    hipError_t e = hipSuccess;
+    if (!b.made) {
+        for (int i = 0; i < 2; ++i)
+            if ((e = hipEventCreateWithFlags(&b.out[i], hipEventDisableTiming)) != hipSuccess) {
+                if (i == 1) (void)hipEventDestroy(b.out[0]);
+                return e;
+            }
+        b.made = true;
+    }
+    if (b.bytes >= bytes) return hipSuccess;
+    for (int i = 0; i < 2; ++i) {
+        if (b.pending[i] && (e = hipEventSynchronize(b.out[i])) != hipSuccess) return e;
+        b.pending[i] = false;
+        if (b.half[i]) (void)hipHostFree(b.half[i]);
+        b.half[i] = nullptr;
+    }
+    b.bytes = 0;
+    for (int i = 0; i < 2; ++i)
+        if ((e = hipHostMalloc(reinterpret_cast<void**>(&b.half[i]), bytes, hipHostMallocDefault)) != hipSuccess) {
+            if (i == 1) (void)hipHostFree(b.half[0]);
+            b.half[0] = b.half[1] = nullptr;
+            return e;
+        }
+    b.bytes = bytes;
+    return hipSuccess;
 }
 
 }  // namespace
@@ -586,14 +693,19 @@ wsr_status wsr_sweep_staged(const wsr_mat* mats, int32_t n, int32_t token, void*
     /* The first copy waits for the work already on `stream` (an earlier reader of the buffer). */
     if ((e = hipEventRecord(ev->start, s)) != hipSuccess || (e = hipStreamWaitEvent(cs, ev->start, 0)) != hipSuccess)
         return hip_fail(e, "sweep_staged: ordering");
-    int64_t k = 0;
-    bool started = false;                            /* the host has waited for `start` */
+    int64_t k = 0, kb = 0;                           /* chunks; chunks through the bounce halves */
+    Bounce* bo = nullptr;
     for (int32_t i = 0; i < n; ++i) {
         const wsr_mat& m = mats[i];
         if (m.M == 0) continue;
         int64_t code_row, scale_row;
         row_parts(m.fmt, m.K, code_row, scale_row);
-        const bool host_wait = pageable(m.w) || (scale_row > 0 && pageable(m.scales));
+        /* a pageable part goes through a pinned bounce half, the others straight to the stage */
+        const bool pw = pageable(m.w), ps = scale_row > 0 && pageable(m.scales);
+        if ((pw || ps) && !bo) {
+            bo = &g_bounce[dev];
+            if ((e = bounce_ready(*bo, (size_t)half)) != hipSuccess) return hip_fail(e, "sweep_staged: pinned bounce");
+        }
         const int64_t per = code_row + scale_row > 0 ? (half - 256) / (code_row + scale_row) : m.M;
         const char* x = static_cast<const char*>(m.x) + (int64_t)token * m.x_tok_stride;
         char* y = reinterpret_cast<char*>(m.y) + (int64_t)token * m.y_tok_stride;
@@ -604,21 +716,33 @@ wsr_status wsr_sweep_staged(const wsr_mat* mats, int32_t n, int32_t token, void*
             /* Buffer b is free once the GEMV of the chunk two back has run. */
             if (k >= 2 && (e = hipStreamWaitEvent(cs, ev->consumed[b], 0)) != hipSuccess)
                 return hip_fail(e, "sweep_staged: wait");
-            if (host_wait) {
-                if (!started && (e = hipEventSynchronize(ev->start)) != hipSuccess)
+            const char* wsrc = static_cast<const char*>(m.w) + r0 * code_row;
+            const char* ssrc = scale_row > 0 ? static_cast<const char*>(m.scales) + r0 * scale_row : nullptr;
+            if (pw || ps) {
+                /* the host fills bounce half bb once its last copy out has run */
+                const int bb = (int)(kb++ & 1);
+                if (bo->pending[bb] && (e = hipEventSynchronize(bo->out[bb])) != hipSuccess)
                     return hip_fail(e, "sweep_staged: host wait");
-                started = true;
-                if (k >= 2 && (e = hipEventSynchronize(ev->consumed[b])) != hipSuccess)
-                    return hip_fail(e, "sweep_staged: host wait");
+                if (pw && rows * code_row > 0) {
+                    CopyPool::get().copy(bo->half[bb], wsrc, (size_t)(rows * code_row));
+                    wsrc = bo->half[bb];
+                }
+                if (ps) {
+                    CopyPool::get().copy(bo->half[bb] + soff, ssrc, (size_t)(rows * scale_row));
+                    ssrc = bo->half[bb] + soff;
+                }
             }
             if (rows * code_row > 0 &&
-                (e = hipMemcpyAsync(buf[b], static_cast<const char*>(m.w) + r0 * code_row, (size_t)(rows * code_row),
-                                    hipMemcpyDefault, cs)) != hipSuccess)
+                (e = hipMemcpyAsync(buf[b], wsrc, (size_t)(rows * code_row), hipMemcpyDefault, cs)) != hipSuccess)
                 return hip_fail(e, "sweep_staged: copy");
             if (scale_row > 0 &&
-                (e = hipMemcpyAsync(buf[b] + soff, static_cast<const char*>(m.scales) + r0 * scale_row,
-                                    (size_t)(rows * scale_row), hipMemcpyDefault, cs)) != hipSuccess)
+                (e = hipMemcpyAsync(buf[b] + soff, ssrc, (size_t)(rows * scale_row), hipMemcpyDefault, cs)) != hipSuccess)
                 return hip_fail(e, "sweep_staged: copy");
+            if (pw || ps) {
+                const int bb = (int)((kb - 1) & 1);
+                if ((e = hipEventRecord(bo->out[bb], cs)) != hipSuccess) return hip_fail(e, "sweep_staged: ordering");
+                bo->pending[bb] = true;
+            }
             if ((e = hipEventRecord(ev->copied[b], cs)) != hipSuccess || (e = hipStreamWaitEvent(s, ev->copied[b], 0)) != hipSuccess)
                 return hip_fail(e, "sweep_staged: ordering");
             const DevMat d = make_devmat(m.fmt, rows, m.K, buf[b], scale_row > 0 ? buf[b] + soff : nullptr, x,
