@@ -549,7 +549,8 @@ bool pageable(const void* p) {
 
 /* Host threads for copies out of pageable memory: copy() splits a range into slices of at least
    4 MiB over up to 8 threads (the calling thread takes one) and returns when all are done.  The
-   threads live for the process (detached, waiting on a condition variable). */
+   threads live for the process (detached, waiting on a condition variable); a process forked from
+   it has none of them, so there the calling thread copies alone. */
 class CopyPool {
 public:
     static CopyPool& get() {
@@ -560,7 +561,7 @@ public:
         std::lock_guard<std::mutex> one(call_mu_);      /* one range at a time */
         constexpr size_t MIN_SLICE = 4u << 20;
         const size_t parts = std::max<size_t>(1, std::min<size_t>(nthreads_ + 1, n / MIN_SLICE));
-        if (parts == 1) {
+        if (parts == 1 || getpid() != pid_) {
             std::memcpy(dst, src, n);
             return;
         }
@@ -587,7 +588,7 @@ private:
         const char* s;
         size_t n;
     };
-    CopyPool() {
+    CopyPool() : pid_(getpid()) {
         const unsigned hw = std::thread::hardware_concurrency();
         nthreads_ = std::max(1u, std::min(8u, hw / 2));
         for (unsigned i = 0; i < nthreads_; ++i) std::thread([this] { run(); }).detach();
@@ -608,6 +609,7 @@ private:
     std::vector<Job> jobs_;
     size_t next_ = 0, left_ = 0;
     unsigned nthreads_ = 1;
+    pid_t pid_;
 };
 
 /* Pinned host halves, per device, through which the staged sweep moves pageable sources: host
