@@ -35,11 +35,17 @@ __device__ __forceinline__ RowRange range_rows(const DevMat& d, int64_t lo, int6
    These loops hand the products to the matrix cores instead.  A wave owns tiles of 16 rows; per
    32-element slab of K it forms D = X^T W^T for the tile with one v_mfma_f32_16x16x32: the A
    operand holds 16 token slots of activations (slots past the pass's tokens repeat its first token
-   and their results are never stored), the B operand 16 weight rows decoded to fp16.  Decoded weights are exact: q4 and int8 codes become the
-   small integers q as 1024 + (q + bias) formed by one bit operation, minus 1024 + bias by one packed
-   fp16 subtraction; 16-bit weights are used as stored.  Every product q x is exact in fp32, and
-   the scales multiply the fp32 slab sums, but the matrix core adds a slab's products in an order of
-   its own, so these results agree with the other loops within rounding, not bit for bit.
+   and their results are never stored), the B operand 16 weight rows decoded to fp16.  Decoded
+   weights are exact.  An int8 code becomes q as 1024 + (q + 128), formed by one bit operation,
+   minus 1024 + 128 by one packed fp16 subtraction.  A q4 code becomes (q + 8) 2^-24, the fp16
+   subnormal whose mantissa is the biased code, formed by one bit operation alone; the bias term
+   8 2^-24 times the slab's activation sum is the same for every row, so one more matrix instruction
+   per slab, with -8 2^-24 in every weight position, gives it for all tiles at once, and it enters
+   each tile's instruction as the accumulator input.  A row group's q4 sums are scaled back by 2^24
+   when stored, which is exact.  16-bit weights are used as stored.  Every product is exact in
+   fp32, and the scales multiply the fp32 slab sums, but the matrix core adds a slab's products in
+   an order of its own, so these results agree with the other loops within rounding, not bit for
+   bit.
    Operand layout (checked on the device): lane i holds A[i%16][8(i/16)+j], B[8(i/16)+j][i%16] and
    D[4(i/16)+j][i%16].  K may be permuted inside a slab as long as A and B follow the same order;
    the decoders give (k0,k4,k1,k5,k2,k6,k3,k7) for a q4 word and (k0,k2,k1,k3,k4,k6,k5,k7) for two
@@ -68,12 +74,16 @@ __device__ __forceinline__ uint32_t f16_sub_bias(uint32_t v, uint32_t neg_bias) 
     return __builtin_bit_cast(uint32_t, __builtin_bit_cast(h2_t, v) + __builtin_bit_cast(h2_t, neg_bias));
 }
 
-/* One q4 code word (code k in nibble k) as 8 fp16 integers, order (k0,k4,k1,k5,k2,k6,k3,k7). */
-__device__ __forceinline__ u32x4 q4_word_f16(uint32_t w) {
-    constexpr uint32_t M = 0x000F000Fu, E = 0x64086408u, NEG = 0xE408E408u;   /* 1024 + (code ^ 8); -1032 */
-    return u32x4{f16_sub_bias((w & M) ^ E, NEG), f16_sub_bias(((w >> 4) & M) ^ E, NEG),
-                 f16_sub_bias(((w >> 8) & M) ^ E, NEG), f16_sub_bias(((w >> 12) & M) ^ E, NEG)};
+/* One q4 code word (code k in nibble k) as 8 fp16 subnormals (q + 8) 2^-24, order
+   (k0,k4,k1,k5,k2,k6,k3,k7): code ^ 8 = q + 8 is the whole mantissa.  Taking the bias out here
+   would cost a packed subtraction per pair; the slab's bias instruction takes it out instead
+   (8B q4 at 16 tokens: 512 -> 386 vector instructions per unit of 64 rows x 256 weights). */
+__device__ __forceinline__ u32x4 q4_word_sub(uint32_t w) {
+    constexpr uint32_t M = 0x000F000Fu, E = 0x00080008u;
+    return u32x4{(w & M) ^ E, ((w >> 4) & M) ^ E, ((w >> 8) & M) ^ E, ((w >> 12) & M) ^ E};
 }
+constexpr uint32_t Q4_NEG_BIAS = 0x80088008u;   /* -8 2^-24 in both fp16 halves  */
+constexpr float Q4_UNSCALE = 0x1p24f;           /* what q4 sums are multiplied by */
 
 /* Two int8 code words (codes k0..k3, k4..k7) as 8 fp16 integers, order (k0,k2,k1,k3,k4,k6,k5,k7). */
 __device__ __forceinline__ u32x4 i8_words_f16(uint32_t w0, uint32_t w1) {
@@ -349,7 +359,9 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
             if constexpr (S_LDS) {
                 if (!scar) read_scales(u, kc);
             }
-            const bool masked = SHORT || e0 < e1;                /* a short row or a moved-back last step */
+            /* a short row or a moved-back last step (never with q4 SCALE16, whose rows are whole
+               steps: known at compile time, the slab loop needs no branch) */
+            const bool masked = SHORT || (!(FMT == FMT_Q4 && SCALE16) && e0 < e1);
             auto slab = [&](int sl) -> u32x4 {
                 u32x4 xs = ring[(sl >> 1) * 2 * WAVE + rd[sl & 1]];
                 if (__builtin_expect(masked, 0)) {
@@ -396,10 +408,11 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
 #pragma unroll
                 for (int sl = 0; sl < SL; ++sl) {                   /* slab sl: block e0 / 32 + sl of each row */
                     const u32x4 xs = x8_q4_order(slab(sl));
-                    f4_t p[NT];
+                    const f4_t bias = mma16<FMT_F16>(xs, u32x4{Q4_NEG_BIAS, Q4_NEG_BIAS, Q4_NEG_BIAS, Q4_NEG_BIAS},
+                                                     f4_t{0.f, 0.f, 0.f, 0.f});
+                    f4_t p[NT];                                  /* 2^-24 q x per row and token */
 #pragma unroll
-                    for (int t = 0; t < NT; ++t)
-                        p[t] = mma16<FMT_F16>(xs, q4_word_f16(u.w[t][sl / 4][sl % 4]), f4_t{0.f, 0.f, 0.f, 0.f});
+                    for (int t = 0; t < NT; ++t) p[t] = mma16<FMT_F16>(xs, q4_word_sub(u.w[t][sl / 4][sl % 4]), bias);
 #pragma unroll
                     for (int t = 0; t < NT; ++t) {
                         if (sl > 0) {
@@ -439,6 +452,7 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
                 const int64_t r = i0 + 16 * t + c;
                 float rs = 1.f;
                 if constexpr (FMT == FMT_I8) rs = f16_bits_to_f32((uint16_t)u.s[t][0]);
+                if constexpr (FMT == FMT_Q4) rs = Q4_UNSCALE;
                 if (r < r1) {
 #pragma unroll
                     for (int jj = 0; jj < 4; ++jj) {
