@@ -20,7 +20,9 @@ CODE = {wl.F16: wsr.WSR_F16, wl.BF16: wsr.WSR_BF16, wl.Q4: wsr.WSR_Q4, wl.I8: ws
 SHAPES = {wl.F16: (100, 520), wl.BF16: (77, 4104), wl.Q4: (100, 2080), wl.I8: (130, 2064)}
 # Matrix-core against vector-ALU outputs: both form every product exactly and sum in fp32, in
 # different orders, so they differ by fp32 rounding only (worst measured on these seeded inputs:
-# 7.0e-6 rel-L2, the 8B q4 down projection with K = 14336; 1e-6 or less for 16-bit and int8).
+# 7.5e-6 rel-L2 per matrix, the 8B q4 down projection with K = 14336, whose q4 products enter the
+# matrix core as (q + 8) x 2^-24 with the bias as accumulator input; 1e-6 or less for 16-bit and
+# int8).
 MMA_VS_VALU = 1e-5
 
 
@@ -252,6 +254,49 @@ def test_mma_edge_cases():
     for t in range(T):
         assert rel_l2(a[t, :M], ora.gemv16(W, X[t], wl.F16)) <= TOL, t
         assert rel_l2(b[t, :24], want_q) <= TOL, t
+
+
+def test_mma_q4_extreme_values():
+    """q4 codes at both ends of their range, block scales from the smallest fp16 subnormal to the
+    largest fp16, activations at +-65504, at the smallest subnormal and mixed: the codes enter the
+    matrix cores as fp16 subnormals (q + 8) 2^-24 and the bias leaves through the accumulator
+    input, which must neither flush nor overflow.  Every token finite and within 2e-3 of the
+    oracle, and every row within the first-order bound of fp32 summation: products are exact, and
+    a result passes through at most 33 roundings in a block (32 products and the bias) and one per
+    block in the row's running sum, each of a partial sum no larger than the sum of the absolute
+    terms, bias terms included (s (|q| + 16) |x| per weight); twice that count of unit roundoffs
+    times that sum bounds the error.  Rows here cancel terms near 65504^2 against each other, so a
+    relative comparison with the vector-ALU sweep means nothing for them (the two paths differ by
+    1.5e-5 rel-L2 on token 5, each within 1.5e-5 of the oracle)."""
+    M, K, T = 64, 1024, 16
+    rng = np.random.default_rng(21)
+    W = synth.q4_codes(M, K, seed=21, stream=611)
+    W[:16] = 0x88                                   # every code -8
+    W[16:32] = 0x77                                 # every code +7
+    svals = synth.encode16([65504.0, 1.0, 2.0 ** -14, 2.0 ** -24, 1e-3], wl.F16)
+    S = svals[rng.integers(0, len(svals), size=(M, K // 32))]
+    X = synth.normal16((T, K), wl.X_SIGMA, wl.F16, seed=21, stream=612)
+    big, nbig, tiny = synth.encode16([65504.0, -65504.0, 2.0 ** -24], wl.F16)
+    X[0], X[1], X[2] = big, nbig, tiny
+    X[3] = synth.encode16(np.where(np.arange(K) % 2 == 0, 1.0, -1.0), wl.F16)
+    for t in range(4, T):
+        idx = rng.permutation(K)[: K // 8]
+        X[t, idx[: K // 16]] = rng.choice(np.array([big, nbig]), size=K // 16)
+        X[t, idx[K // 16:]] = tiny
+    y = run_mma(wl.Q4, W, S, X, M, K, T)
+    nib = np.stack([W & 0xF, W >> 4], axis=-1).reshape(M, K).astype(np.int64)   # even k low nibble
+    q = (nib ^ 8) - 8
+    sk = np.repeat(S.view(np.float16).astype(np.float64), 32, axis=1)
+    mag = sk * (np.abs(q) + 16)                       # per weight: s (|q| + 16)
+    rounds = 2 * (33 + K // 32)
+    ora = oracle.get()
+    for t in range(T):
+        want = ora.gemv(dict(fmt=wl.Q4, w=W, s=S), X[t])
+        assert np.isfinite(y[t]).all(), t
+        assert rel_l2(y[t], want) <= TOL, t
+        bound = rounds * 2.0 ** -24 * (mag @ np.abs(X[t].view(np.float16).astype(np.float64)))
+        bound += 2.0 ** -24 * np.abs(want.astype(np.float64))           # the oracle's fp32 result
+        assert (np.abs(y[t].astype(np.float64) - want.astype(np.float64)) <= bound).all(), t
 
 
 def test_mma_mixed_full_size_tail():
