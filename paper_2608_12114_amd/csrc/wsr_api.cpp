@@ -548,9 +548,9 @@ bool pageable(const void* p) {
 }
 
 /* Host threads for copies out of pageable memory: copy() splits a range into slices of at least
-   4 MiB over up to 8 threads (the calling thread takes one) and returns when all are done.  The
-   threads live for the process (detached, waiting on a condition variable); a process forked from
-   it has none of them, so there the calling thread copies alone. */
+   4 MiB over the calling thread and up to 8 helpers and returns when all are done.  The helpers
+   live for the process (detached, waiting on a condition variable); a process forked from it has
+   none of them, so there, as where no helper could be started, the calling thread copies alone. */
 class CopyPool {
 public:
     static CopyPool& get() {
@@ -558,13 +558,14 @@ public:
         return *p;
     }
     void copy(char* dst, const char* src, size_t n) {
-        std::lock_guard<std::mutex> one(call_mu_);      /* one range at a time */
         constexpr size_t MIN_SLICE = 4u << 20;
         const size_t parts = std::max<size_t>(1, std::min<size_t>(nthreads_ + 1, n / MIN_SLICE));
+        /* a forked process takes none of the locks: one may have been held when it was forked */
         if (parts == 1 || getpid() != pid_) {
             std::memcpy(dst, src, n);
             return;
         }
+        std::lock_guard<std::mutex> one(call_mu_);      /* one range at a time */
         const size_t per = (n + parts - 1) / parts;
         {
             std::lock_guard<std::mutex> l(mu_);
@@ -590,8 +591,13 @@ private:
     };
     CopyPool() : pid_(getpid()) {
         const unsigned hw = std::thread::hardware_concurrency();
-        nthreads_ = std::max(1u, std::min(8u, hw / 2));
-        for (unsigned i = 0; i < nthreads_; ++i) std::thread([this] { run(); }).detach();
+        const unsigned want = std::max(1u, std::min(8u, hw / 2));
+        unsigned made = 0;
+        try {                                            /* no exception may leave the C ABI */
+            for (; made < want; ++made) std::thread([this] { run(); }).detach();
+        } catch (...) {
+        }
+        nthreads_ = made;                                /* 0: the calling thread copies alone */
     }
     void run() {
         std::unique_lock<std::mutex> l(mu_);
@@ -608,7 +614,7 @@ private:
     std::condition_variable cv_, done_;
     std::vector<Job> jobs_;
     size_t next_ = 0, left_ = 0;
-    unsigned nthreads_ = 1;
+    unsigned nthreads_ = 0;
     pid_t pid_;
 };
 
