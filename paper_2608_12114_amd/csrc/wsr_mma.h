@@ -162,7 +162,7 @@ __device__ __forceinline__ u32x4 keep_if(bool ok, u32x4 v) { return ok ? v : zer
    memory into a two-unit ring in the wave's LDS and are read back slab by slab as they are
    multiplied (8B q4 at 16 tokens 13.7k -> 14.1k tok/s, int8 protocol 74.7k -> 80.8k, 70B bf16
    +0.5 to +0.9 %).  Where a step's eight q4 block scales of a row are one aligned 16-byte run
-   (SCALE16), the scales of MMA_SCALE_STEPS steps of the group's rows come into LDS at once, one
+   (WHOLE), the scales of MMA_SCALE_STEPS steps of the group's rows come into LDS at once, one
    load of 64 lanes per 16 rows (64 contiguous bytes of each row), where loading a step's scales
    into registers took one instruction per tile, each returning the same 16 bytes of a row to all
    four lane groups, and touched a cache line per row per step (8B q4 at 16 tokens: 15.7k ->
@@ -192,13 +192,15 @@ __device__ __forceinline__ void wait_vm() {
    is not a whole number of steps, its last step is moved back to end at the row's end and the
    values the previous step already covered are zeroed when it is multiplied (masking them as they
    arrive would make each load wait at once).  Rows shorter than one step (SHORT) clamp each
-   lane's offset instead.  Where q4 rows hold a whole number of 8-block steps and the scales are
-   16-byte aligned (SCALE16), a step's eight block scales of a row are one 16-byte run and come
-   through LDS in blocks of four steps (below); otherwise each is loaded into registers alone.
+   lane's offset instead.  Where rows hold a whole number of steps (WHOLE), no step is ever moved
+   back and the loop carries no mask (16-bit and int8: the mask's selects cost 40 % of a 16-bit
+   unit's vector instructions).  For q4, WHOLE also asks for 16-byte aligned scales: a step's
+   eight block scales of a row are then one 16-byte run and come through LDS in blocks of four
+   steps (below); otherwise each is loaded into registers alone.
    The caller keeps 16 NT rows of codes and 16 tokens of activations within 2^31 bytes.  The
-   activations (and, with SCALE16, the q4 scales) come from the LDS ring, which leaves the register
+   activations (and, with WHOLE, the q4 scales) come from the LDS ring, which leaves the register
    ring to the weights. */
-template <int FMT, int NT, bool SCALE16, bool SHORT>
+template <int FMT, int NT, bool WHOLE, bool SHORT>
 __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1, int32_t token0, int ntok, int lane,
                                          u32x4* __restrict__ xlds) {
     using Unit = MmaUnit<FMT, NT>;
@@ -222,13 +224,13 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
     int lbuf = 0, mbuf = 0;                                      /* LDS ring half of the next load, multiply */
     rsrc_t rw = buffer_of(d.w), rs = buffer_of(d.w);             /* this group's row r0 of codes, scales */
     uint32_t vr[NT], vs[NT];                                     /* lane offsets: row of each tile */
-    /* q4 SCALE16: the block of scales of steps 4 m .. 4 m + 3 of the group's 16 NT rows comes into
+    /* q4 WHOLE: the block of scales of steps 4 m .. 4 m + 3 of the group's 16 NT rows comes into
        LDS with the first of those steps, NT loads of 16 rows each: lane i of load j brings row
        r = 16 j + i / 4 at step 4 m + ((i % 4) ^ (r / 2 % 4)), into block slot 4 r + i % 4 (the
        rotation spreads a tile's 16 rows of one step over the LDS banks).  The block is overwritten
        when the next one comes, one unit before the old block's last unit is multiplied, so that
        unit's scales are read into its registers at the end of the unit before it (scar). */
-    constexpr bool S_LDS = FMT == FMT_Q4 && SCALE16;
+    constexpr bool S_LDS = FMT == FMT_Q4 && WHOLE;
     constexpr int NBD = S_LDS ? NT : 0;                          /* loads of a scale block */
     constexpr int SBLK = 2 * SL * WAVE;                          /* the block's first slot */
     uint32_t vsb[NBD > 0 ? NBD : 1] = {};                        /* row 16 j + i / 4 of lane i, load j */
@@ -313,7 +315,7 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             if constexpr (FMT == FMT_Q4) {
-                if constexpr (!SCALE16) {                        /* (SCALE16: in the LDS ring) */
+                if constexpr (!WHOLE) {                          /* (WHOLE: in the LDS ring) */
                     uint32_t h[8];
 #pragma unroll
                     for (int j = 0; j < 8; ++j) h[j] = buf_u16(rs, vs[t], (uint32_t)std::min<int64_t>(b0 + j, nc - 1) * 2);
@@ -329,7 +331,7 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
     /* Vector memory operations each load() issues after its loads into LDS (weights, scales; the
        int8 row scales, loaded on a group's last step only, are left out: a wait that counts fewer
        later loads than were issued still covers the ring). */
-    constexpr int AFTER_X = NT * J + (FMT == FMT_Q4 ? (SCALE16 ? 0 : 8 * NT) : 0);
+    constexpr int AFTER_X = NT * J + (FMT == FMT_Q4 ? (WHOLE ? 0 : 8 * NT) : 0);
     constexpr int PER_UNIT = SL + AFTER_X;                       /* plus NBD where a scale block starts */
     auto multiply = [&](Unit& u, Unit& un, auto next_loaded) {   /* un: the next unit's registers */
         const int64_t i0 = r0 + gc * 16 * NT;
@@ -359,9 +361,8 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
             if constexpr (S_LDS) {
                 if (!scar) read_scales(u, kc);
             }
-            /* a short row or a moved-back last step (never with q4 SCALE16, whose rows are whole
-               steps: known at compile time, the slab loop needs no branch) */
-            const bool masked = SHORT || (!(FMT == FMT_Q4 && SCALE16) && e0 < e1);
+            /* a short row or a moved-back last step (never with WHOLE: known at compile time) */
+            const bool masked = SHORT || (!WHOLE && e0 < e1);
             auto slab = [&](int sl) -> u32x4 {
                 u32x4 xs = ring[(sl >> 1) * 2 * WAVE + rd[sl & 1]];
                 if (__builtin_expect(masked, 0)) {
@@ -420,7 +421,7 @@ __device__ __forceinline__ void rows_mma(const DevMat& d, int64_t r0, int64_t r1
                             __asm__ volatile("" : "+v"(acc[t]));
                         }
                         float sc = f16_bits_to_f32((uint16_t)(u.s[t][sl / 2] >> (16 * (sl % 2))));
-                        if constexpr (!SCALE16) {
+                        if constexpr (!WHOLE) {
                             const int64_t b = e0 / 32 + sl;
                             sc = b >= e1 / 32 && b < nc ? sc : 0.f;
                         }
@@ -520,19 +521,26 @@ __device__ __forceinline__ void stream_range_mma(const DevMat* __restrict__ tab,
         }
         if (rr.r0 >= rr.r1) continue;
         const bool short_rows = d.nc * 16 < 128;                 /* under one step */
-#define WSR_ROWS(F, S16, SH) rows_mma<F, NT, S16, SH>(d, rr.r0, rr.r1, token0, ntok, lane, xlds)
+#define WSR_ROWS(F, W, SH) rows_mma<F, NT, W, SH>(d, rr.r0, rr.r1, token0, ntok, lane, xlds)
+        const bool whole = d.nc % 8 == 0;                        /* 128-byte steps: 8 chunks or blocks */
         if constexpr (FMT == FMT_Q4_WHOLE) {                     /* the launcher checked every matrix */
             WSR_ROWS(FMT_Q4, true, false);
         } else if ((F == 0 || F == FMT_F16) && fmt == FMT_F16) {
-            if (short_rows) WSR_ROWS(FMT_F16, false, true); else WSR_ROWS(FMT_F16, false, false);
+            if (short_rows) WSR_ROWS(FMT_F16, false, true);
+            else if (whole) WSR_ROWS(FMT_F16, true, false);
+            else WSR_ROWS(FMT_F16, false, false);
         } else if ((F == 0 || F == FMT_BF16) && fmt == FMT_BF16) {
-            if (short_rows) WSR_ROWS(FMT_BF16, false, true); else WSR_ROWS(FMT_BF16, false, false);
+            if (short_rows) WSR_ROWS(FMT_BF16, false, true);
+            else if (whole) WSR_ROWS(FMT_BF16, true, false);
+            else WSR_ROWS(FMT_BF16, false, false);
         } else if ((F == 0 || F == FMT_Q4) && fmt == FMT_Q4) {
             if (short_rows) WSR_ROWS(FMT_Q4, false, true);
-            else if (d.nc % 8 == 0 && (reinterpret_cast<uintptr_t>(d.s) & 15) == 0) WSR_ROWS(FMT_Q4, true, false);
+            else if (whole && (reinterpret_cast<uintptr_t>(d.s) & 15) == 0) WSR_ROWS(FMT_Q4, true, false);
             else WSR_ROWS(FMT_Q4, false, false);
         } else if ((F == 0 || F == FMT_I8) && fmt == FMT_I8) {
-            if (short_rows) WSR_ROWS(FMT_I8, false, true); else WSR_ROWS(FMT_I8, false, false);
+            if (short_rows) WSR_ROWS(FMT_I8, false, true);
+            else if (whole) WSR_ROWS(FMT_I8, true, false);
+            else WSR_ROWS(FMT_I8, false, false);
         }
 #undef WSR_ROWS
     }
