@@ -957,6 +957,24 @@ def across_processes(args):
                       "GBps_at_median": round(bpt / (st["median"] * 1e-3) / 1e9, 2)}), flush=True)
 
 
+def measured_ceiling(head_gbps, rows):
+    """The second denominator: the streaming-read probe's resident rate measured in this run (the
+    pure-read reference), against which the headline and every row's roofline rate are also given
+    (`frac_of_probe`, added to each row).  The probe's timed passes are 1 GiB each (two launches),
+    where a 70B sweep token is one launch over 139 GB, so a long sweep can pass it slightly."""
+    if "probe" not in rows:
+        return None
+    pc = rows["probe"]["resident_GBps"]
+    for key, r in rows.items():
+        rl = r.get("roofline") if isinstance(r, dict) else None
+        if rl and rl.get("achieved") and key != "probe":
+            r["frac_of_probe"] = round(rl["achieved"] / pc, 4)
+    return {"GBps": round(pc, 1), "frac": round(head_gbps / pc, 4),
+            "source": "rows.probe.resident_GBps: 1 GiB fp32 probe, four buffers rotated, back to back",
+            "note": "probe passes are 1 GiB (two launches each); the sweep token is one launch over all its "
+                    "bytes, so its ramp and drain weigh less and the fraction can exceed 1"}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -1002,6 +1020,7 @@ def main():
             raise SystemExit(f"unknown row {r}")
 
     gbps = head["GBps"]
+    probe_ceiling = measured_ceiling(gbps, rows)
     dtype = {"llama70b_bf16": "bf16", "llama8b_q4": "q4+f16"}[args.workload]
     traffic, traffic_src = profiled_traffic(args.workload)
     line = {
@@ -1018,6 +1037,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(gbps, 2), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
                      "frac": round(head["hbm_frac"], 4), "traffic": traffic, "traffic_source": traffic_src,
                      "kernel": f"k_sweep ({dtype})", "bytes_per_launch": head["bytes_per_token"]},
+        "probe_ceiling": probe_ceiling,
         "cpu_baseline": head.get("cpu_baseline"),
         "parity": head["parity"],
         "passes": head["passes"],

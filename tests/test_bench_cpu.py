@@ -92,3 +92,14 @@ def test_probe_and_gemv_oracle_baselines_on_small_inputs():
     x = synth.normal16(256, 1.0, "f16", seed=0, stream=9)
     g = bench.gemv_cpu_baseline(W, x, "f16", 0.05, "three small matrices")
     assert g["value"] > 0 and g["single_thread"]["calls"] >= 1 and g["sample"].startswith("three small")
+
+
+def test_measured_ceiling_second_denominator():
+    rows = {"probe": {"resident_GBps": 7000.0, "roofline": {"achieved": 7000.0}},
+            "gemv_f16": {"roofline": {"achieved": 3500.0}},
+            "endpoints": {"GBps": {"resident": 1.0}}}
+    pc = bench.measured_ceiling(7140.0, rows)
+    assert pc["GBps"] == 7000.0 and pc["frac"] == 1.02
+    assert rows["gemv_f16"]["frac_of_probe"] == 0.5
+    assert "frac_of_probe" not in rows["probe"] and "frac_of_probe" not in rows["endpoints"]
+    assert bench.measured_ceiling(7140.0, {"gemv_f16": {"roofline": {"achieved": 1.0}}}) is None
