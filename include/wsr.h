@@ -219,10 +219,13 @@ wsr_status wsr_decode_sweep_noalloc(const wsr_mat* mats, int32_t n, int32_t n_to
    wsr_decode_sweep_mma: for t < n_tokens and every matrix m, y_m(t) = W_m . x_m(t) as in
    wsr_decode_sweep, with up to 16 tokens per pass over the weights and the products formed by the
    matrix cores (v_mfma_f32_16x16x32): each 16-row, 16-token tile accumulates slabs of 32 weights,
-   decoded to exact fp16 integers for q4 and int8 and used as stored for fp16 and bf16.  Every
-   product is exact and sums are fp32, but a slab's products are added in the matrix core's own
-   order, so outputs agree with wsr_decode_sweep within rounding (not bit for bit); a unit
-   activation vector still returns the dequantised weights exactly.  Tokens go in passes of 16, the
+   used as stored for fp16 and bf16, decoded to exact fp16 integers for int8, and for q4 to the
+   exact fp16 subnormals (q + 8) 2^-24 with the bias removed by one more matrix instruction per
+   slab and the sums scaled back by 2^24.  Every product is exact and sums are fp32, but a slab's
+   products are added in the matrix core's own order, so outputs agree with wsr_decode_sweep within
+   rounding (not bit for bit: relative L2 within 1e-5 per matrix over 16 tokens on the tested
+   models, up to about 1.2e-5 for single tokens of 14,336-long q4 rows); a unit activation vector
+   still returns the dequantised weights exactly.  Tokens go in passes of 16, the
    last pass holding the rest.  A pass of a single token (n_tokens = 1, or a last pass of one) runs
    the vector-ALU loop of wsr_decode_sweep instead, whose outputs it then equals bit for bit: a
    matrix instruction would compute 16 token slots to use one.  Formats, layouts, flags and the workspace as for wsr_decode_sweep;
