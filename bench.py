@@ -432,13 +432,17 @@ def row_probe(stream, wsr, mapped=True, want_cpu=True):
     # host-mapped: the same kernel over pinned host pages read in place across PCIe
     host = torch.empty(nb, dtype=torch.uint8, pin_memory=True)
     synth.grid_f32(n, seed=0, stream=1, out=host.numpy().view(np.float32))
+    t_reg = time.perf_counter()
     dev, granted = wsr.wsr_register_host(host, nb, 0)
+    res["mapped_register_s"] = time.perf_counter() - t_reg      # setup, outside the rate
     try:
         call(dev)
         mapped = median_of(lambda: call(dev), 2, 3, stream) / 2
         res.update({"mapped_GBps": nb / mapped / 1e9, "mapped_registration": granted})
     finally:
+        t_unreg = time.perf_counter()
         wsr.wsr_unregister_host(host)
+        res["mapped_unregister_s"] = time.perf_counter() - t_unreg
     log(f"probe: resident {res['resident_GBps']:.1f} GB/s (same buffer {res['resident_same_buffer_GBps']:.1f}), "
         f"host-mapped {res['mapped_GBps']:.1f} GB/s")
     return res
@@ -672,7 +676,9 @@ def row_endpoints(stream, wsr, warmup=2, passes=5, stage_mib=64):
         # map arm: the same bytes read in place from pinned host pages, adopted through registration
         pinned = torch.empty((W + page - 1) // page * page, dtype=torch.uint8, pin_memory=True)
         pinned.numpy()[:W] = fmap
+        t_reg = time.perf_counter()
         dview, granted = wsr.wsr_register_host(pinned, pinned.numel(), 0)
+        res["register_s"] = time.perf_counter() - t_reg           # setup, outside every rate (a1)
         try:
             sp_map = specs(dview, "map")
             t_map = timed_arm(lambda: wsr.wsr_decode_sweep(sp_map, 1, ws, ws.numel(), stream))
@@ -686,7 +692,9 @@ def row_endpoints(stream, wsr, warmup=2, passes=5, stage_mib=64):
             t_cp = timed_arm(lambda: wsr.wsr_sweep_staged(sp_cp, 0, stage, stage.numel(), stream, cs))
             torch.cuda.synchronize()
         finally:
+            t_unreg = time.perf_counter()
             wsr.wsr_unregister_host(pinned)
+            res["unregister_s"] = time.perf_counter() - t_unreg
         same = all(torch.equal(ys["resident"][i], ys[a][i]) for a in ("map", "copy_file", "copy_pinned")
                    for i in range(len(mats)))
         # step 5: the mapping after one pass of every arm

@@ -61,7 +61,7 @@ def _run(cmd):
     return r
 
 
-KERNEL_FILES = ("wsr_kernels.hip", "wsr_mma.hip")
+KERNEL_FILES = ("wsr_kernels.hip", "wsr_mma.hip", "wsr_copy.hip")
 
 
 def _compile_kernels(src: str) -> str:

@@ -18,6 +18,7 @@
 #include <vector>
 
 #include "wsr.h"
+#include "wsr_copy.h"
 #include "wsr_internal.h"
 #include "wsr_mma_launch.h"
 
@@ -109,30 +110,44 @@ bool inside(const void* p, size_t bytes, const void* start, size_t size) {
     return a >= s0 && a - s0 <= size && bytes <= size - (a - s0);
 }
 
-/* The extent of the pinned allocation that holds `host` (device view `dev`) must cover the whole
- * requested range.  The runtime is asked for the allocation's range through the host address and,
- * if that gives no answer, through the device address; a range it cannot bound is refused. */
-wsr_status check_pinned_extent(const void* host, const void* dev, size_t bytes) {
+/* Whether the pinned allocation that holds `host` (device view `dev`) covers [host, host + bytes):
+ * 1 yes, 0 the range runs past its end, -1 the runtime reports no extent.  The runtime is asked for
+ * the allocation's range through the host address and, if that gives no answer, through the device
+ * address.  *start and *size receive the extent found (for messages). */
+int pinned_extent_covers(const void* host, const void* dev, size_t bytes, const void** start_out, size_t* size_out) {
     void* start = nullptr;
     size_t size = 0;
     hipDeviceptr_t hp = const_cast<void*>(host);
     if (hipPointerGetAttribute(&start, HIP_POINTER_ATTRIBUTE_RANGE_START_ADDR, hp) == hipSuccess &&
         hipPointerGetAttribute(&size, HIP_POINTER_ATTRIBUTE_RANGE_SIZE, hp) == hipSuccess && size > 0 &&
         inside(host, 1, start, size)) {
-        if (inside(host, bytes, start, size)) return WSR_OK;
-        return fail(WSR_E_SIZE, "register_host: %p + %zu runs past the end of its pinned allocation "
-                    "(%p + %zu)", host, bytes, start, size);
+        *start_out = start;
+        *size_out = size;
+        return inside(host, bytes, start, size) ? 1 : 0;
     }
     (void)hipGetLastError();
     hipDeviceptr_t base = nullptr;
     size = 0;
     if (hipMemGetAddressRange(&base, &size, const_cast<void*>(dev)) == hipSuccess && size > 0 &&
         inside(dev, 1, base, size)) {
-        if (inside(dev, bytes, base, size)) return WSR_OK;
-        return fail(WSR_E_SIZE, "register_host: %p + %zu runs past the end of its pinned allocation "
-                    "(device range %p + %zu)", host, bytes, base, size);
+        *start_out = base;
+        *size_out = size;
+        return inside(dev, bytes, base, size) ? 1 : 0;
     }
     (void)hipGetLastError();
+    return -1;
+}
+
+/* The extent of the pinned allocation that holds `host` must cover the whole requested range; a
+ * range the runtime cannot bound is refused. */
+wsr_status check_pinned_extent(const void* host, const void* dev, size_t bytes) {
+    const void* start = nullptr;
+    size_t size = 0;
+    const int c = pinned_extent_covers(host, dev, bytes, &start, &size);
+    if (c == 1) return WSR_OK;
+    if (c == 0)
+        return fail(WSR_E_SIZE, "register_host: %p + %zu runs past the end of its pinned allocation "
+                    "(%p + %zu)", host, bytes, start, size);
     return fail(WSR_E_UNSUPPORTED, "register_host: the runtime does not report the extent of the pinned "
                 "allocation holding %p, so the range cannot be checked", host);
 }
@@ -536,6 +551,22 @@ hipError_t make_stage_events(StageEvents& e) {
     return hipSuccess;
 }
 
+/* The device view of [p, p + bytes) where all of it lies in one pinned host allocation, else null
+   (pageable or device memory, or an extent the runtime does not report). */
+const char* pinned_view(const void* p, size_t bytes) {
+    if (!p || bytes == 0) return nullptr;
+    hipPointerAttribute_t a{};
+    if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    if (a.type != hipMemoryTypeHost || a.devicePointer == nullptr) return nullptr;
+    const void* start = nullptr;
+    size_t size = 0;
+    return pinned_extent_covers(p, a.devicePointer, bytes, &start, &size) == 1 ? static_cast<const char*>(a.devicePointer)
+                                                                               : nullptr;
+}
+
 /* True for host memory the runtime has not registered (pageable). */
 bool pageable(const void* p) {
     if (!p) return false;
@@ -626,6 +657,7 @@ private:
    staged sweep's per-device mutex guards them. */
 struct Bounce {
     char* half[2] = {nullptr, nullptr};
+    char* view[2] = {nullptr, nullptr};                  /* their device views (null: copy with the runtime) */
     size_t bytes = 0;
     hipEvent_t out[2]{};                                 /* the last copy out of each half */
     bool pending[2] = {false, false};
@@ -648,7 +680,7 @@ hipError_t bounce_ready(Bounce& b, size_t bytes) {
         if (b.pending[i] && (e = hipEventSynchronize(b.out[i])) != hipSuccess) return e;
         b.pending[i] = false;
         if (b.half[i]) (void)hipHostFree(b.half[i]);
-        b.half[i] = nullptr;
+        b.half[i] = b.view[i] = nullptr;
     }
     b.bytes = 0;
     for (int i = 0; i < 2; ++i)
@@ -657,8 +689,22 @@ hipError_t bounce_ready(Bounce& b, size_t bytes) {
             b.half[0] = b.half[1] = nullptr;
             return e;
         }
+    for (int i = 0; i < 2; ++i) {
+        void* v = nullptr;
+        if (hipHostGetDevicePointer(&v, b.half[i], 0) == hipSuccess) b.view[i] = static_cast<char*>(v);
+        else (void)hipGetLastError();
+    }
     b.bytes = bytes;
     return hipSuccess;
+}
+
+/* One part of a chunk into the stage on the copy stream: by the shaders from the source's device
+   view where it has one and 16-byte alignment allows, else by the runtime. */
+hipError_t stage_copy(char* dst, const char* src, const char* src_view, size_t bytes, hipStream_t cs) {
+    if (bytes == 0) return hipSuccess;
+    if (src_view && ((reinterpret_cast<uintptr_t>(src_view) | reinterpret_cast<uintptr_t>(dst) | bytes) & 15) == 0)
+        return wsr::launch_copy16(src_view, dst, bytes, cs);
+    return hipMemcpyAsync(dst, src, bytes, hipMemcpyDefault, cs);
 }
 
 }  // namespace
@@ -708,8 +754,12 @@ wsr_status wsr_sweep_staged(const wsr_mat* mats, int32_t n, int32_t token, void*
         if (m.M == 0) continue;
         int64_t code_row, scale_row;
         row_parts(m.fmt, m.K, code_row, scale_row);
-        /* a pageable part goes through a pinned bounce half, the others straight to the stage */
+        /* a pageable part goes through a pinned bounce half, the others straight to the stage; the
+           shaders copy what is in pinned host pages (the copy engines halved that rate in some
+           processes), the runtime the rest */
         const bool pw = pageable(m.w), ps = scale_row > 0 && pageable(m.scales);
+        const char* wview = pw ? nullptr : pinned_view(m.w, (size_t)(m.M * code_row));
+        const char* sview = ps || scale_row == 0 ? nullptr : pinned_view(m.scales, (size_t)(m.M * scale_row));
         if ((pw || ps) && !bo) {
             bo = &g_bounce[dev];
             if ((e = bounce_ready(*bo, (size_t)half)) != hipSuccess) return hip_fail(e, "sweep_staged: pinned bounce");
@@ -726,6 +776,8 @@ wsr_status wsr_sweep_staged(const wsr_mat* mats, int32_t n, int32_t token, void*
                 return hip_fail(e, "sweep_staged: wait");
             const char* wsrc = static_cast<const char*>(m.w) + r0 * code_row;
             const char* ssrc = scale_row > 0 ? static_cast<const char*>(m.scales) + r0 * scale_row : nullptr;
+            const char* wdev = wview ? wview + r0 * code_row : nullptr;       /* device views, if pinned */
+            const char* sdev = sview ? sview + r0 * scale_row : nullptr;
             if (pw || ps) {
                 /* the host fills bounce half bb once its last copy out has run */
                 const int bb = (int)(kb++ & 1);
@@ -734,17 +786,17 @@ wsr_status wsr_sweep_staged(const wsr_mat* mats, int32_t n, int32_t token, void*
                 if (pw && rows * code_row > 0) {
                     CopyPool::get().copy(bo->half[bb], wsrc, (size_t)(rows * code_row));
                     wsrc = bo->half[bb];
+                    wdev = bo->view[bb];
                 }
                 if (ps) {
                     CopyPool::get().copy(bo->half[bb] + soff, ssrc, (size_t)(rows * scale_row));
                     ssrc = bo->half[bb] + soff;
+                    sdev = bo->view[bb] ? bo->view[bb] + soff : nullptr;
                 }
             }
-            if (rows * code_row > 0 &&
-                (e = hipMemcpyAsync(buf[b], wsrc, (size_t)(rows * code_row), hipMemcpyDefault, cs)) != hipSuccess)
+            if ((e = stage_copy(buf[b], wsrc, wdev, (size_t)(rows * code_row), cs)) != hipSuccess)
                 return hip_fail(e, "sweep_staged: copy");
-            if (scale_row > 0 &&
-                (e = hipMemcpyAsync(buf[b] + soff, ssrc, (size_t)(rows * scale_row), hipMemcpyDefault, cs)) != hipSuccess)
+            if (scale_row > 0 && (e = stage_copy(buf[b] + soff, ssrc, sdev, (size_t)(rows * scale_row), cs)) != hipSuccess)
                 return hip_fail(e, "sweep_staged: copy");
             if (pw || ps) {
                 const int bb = (int)((kb - 1) & 1);

@@ -13,6 +13,7 @@ import synth
 KERNEL_SOURCES = [
     (os.path.join(wb.CSRC, "wsr_kernels.hip"), [*wb.COMMON, *wb.DEVICE]),
     (os.path.join(wb.CSRC, "wsr_mma.hip"), [*wb.COMMON, *wb.DEVICE]),
+    (os.path.join(wb.CSRC, "wsr_copy.hip"), [*wb.COMMON, *wb.DEVICE]),
     (synth.DEV_SRC_PATH, ["-O3", "--offload-arch=gfx950", "-ffp-contract=off",
                           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]),
 ]
