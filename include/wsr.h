@@ -271,8 +271,11 @@ wsr_status wsr_decode_sweep_ordered(const wsr_mat* mats, int32_t n, int32_t n_to
    `stream`.  Use distinct streams for overlap (the same stream also works, serially).  The source
    memory must stay valid and unchanged until the copies have run.  Pageable host sources go
    through two pinned host halves the library keeps per device (each the size of a stage half):
-   host threads copy a chunk into one half while the DMA engine moves the previous chunk out of
-   the other, so for such sources the call blocks until its last chunk is in a pinned half.  mats: as wsr_decode_sweep, except that w and scales may
+   host threads copy a chunk into one half while the previous chunk moves out of the other, so for
+   such sources the call blocks until its last chunk is in a pinned half.  Chunks in pinned host
+   pages (a bounce half, or a caller's matrix that lies wholly in one pinned allocation) with
+   16-byte aligned ends are copied by a kernel of the library on copy_stream, which reads them
+   across PCIe; other chunks by hipMemcpyAsync on copy_stream.  mats: as wsr_decode_sweep, except that w and scales may
    be host pointers; x and y device memory.  WSR_E_SIZE if half of stage_bytes, less 256, holds no
    row of some matrix.  Calls on one device are serialised while they enqueue (events shared per
    device). */
