@@ -297,7 +297,7 @@ def oracle_gemv(ora, fmt, hw, x, threads=1):
 
 def oracle_threads():
     """Host threads for the oracle's all-core mode: every core this process may run on, capped by
-    OMP_NUM_THREADS where that is set lower (a GPU machine grants the process a share of its cores).
+    OMP_NUM_THREADS where that is set lower (a machine may grant the process only a share of its cores).
     Returns (threads used, cores available, the cap's source or None)."""
     try:
         avail = len(os.sched_getaffinity(0))

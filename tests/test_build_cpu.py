@@ -82,7 +82,7 @@ def _source_files():
         return [p for p in r.stdout.decode().split("\0") if p]
     out = []
     for d, dirs, files in os.walk(_ROOT):
-        dirs[:] = [x for x in dirs if x not in (".git", "_work", "_build", "gpurun_out", "__pycache__")]
+        dirs[:] = [x for x in dirs if not x.startswith((".", "_")) and not x.endswith("_out")]   # working folders
         out += [os.path.relpath(os.path.join(d, f), _ROOT) for f in files
                 if not f.endswith((".so", ".o", ".pyc"))]
     return out
